@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Benchmark of the sparse-prefill evidence probe on one MI355X.
+
+Workload: 28 independent layers (fresh seeded Q, K, V per layer), 28 query
+heads / 4 kv heads, head dim 128, bf16; one video of 256 frames x 64 visual
+tokens followed by 128 query tokens (16,512 tokens); block-sparse rule: sink
+block + 8 preceding blocks + own block for visual rows, query rows dense over
+all visual blocks; 16 planted frames.
+
+One step = the whole probe: for each of the 28 layers one
+evisel_sparse_prefill call (attention with fused evidence partials, split-row
+combine, evidence reduction), then one evisel_frame_evidence call (head/layer
+aggregation and top-16 frames). Inputs are resident in HBM before timing.
+
+Prints one JSON line: probe tokens/s (value), ms per step, the attention
+kernel's roofline against the bf16 MFMA peak (active-block FLOPs over the
+kernel's HIP-event time, measured over the timed region), and the fp64 CPU
+oracle's throughput on a bounded sample (one full layer) as a baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 flop/clk (dense)
+PEAK_HBM_GBS = 8000.0
+
+
+def _world():
+    return int(os.environ.get("WORLD_SIZE", "1")), int(os.environ.get("RANK",
+                                                                      "0"))
+
+
+def cpu_baseline(w, seed=0):
+    """The fp64 oracle (as it stands) on one full layer: all rows' output
+    and LSE plus the evidence of all query rows. Scaled to probe tokens/s
+    for the whole L-layer probe."""
+    import numpy as np
+    import oracle
+    from oracle.layout import Layout, Rule
+    import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(i["num_threads"] for i in threadpool_info())
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    lay = Layout(ns, nf, nt, w.tokens_per_frame)
+    rule = Rule(w.block, w.sink_blocks, w.window)
+    q, k, v = wl.gen_layer(w, 0, seed).as_f64()
+    t0 = time.perf_counter()
+    oracle.run_layer(q, k, v, lay, rule, w.softmax_scale)
+    dt = time.perf_counter() - t0
+    return {"value": lay.S / (dt * w.n_layers), "unit": "tokens/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"layer 0 of {w.n_layers}, all {lay.S} rows x {w.hq} "
+                      f"heads + evidence ({dt:.1f} s), scaled to "
+                      f"{w.n_layers} layers",
+            "host_cpus": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world, rank = _world()
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the probe is not sharded "
+              "across GPUs in this library (run with --gpus 1).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as wl
+    import paper_2608_05780_amd as ev
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    ev.load()
+    torch.cuda.set_device(0)
+    w = wl.get(args.config)
+    L = w.n_layers
+    ns, nf, nt = wl.layout_arrays(w, args.seed)
+    _, core, _ = wl.plant_table(w, args.seed)
+    ks = []
+    off = 0
+    for F in nf:
+        ks.append(int(((core >= off) & (core < off + F)).sum()))
+        off += int(F)
+
+    mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
+                               w.sink_blocks, w.window, w.hq, w.hkv, n_sys=ns)
+    st = mask.stats
+    S, T = st["n_tokens"], st["n_frames_total"]
+    print(f"# {w.name}: S={S} T={T} active pairs/head/layer="
+          f"{st['n_active_pairs']} items={st['n_work_items']}",
+          file=sys.stderr, flush=True)
+
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    qs, kks, vs = [], [], []
+    t0 = time.time()
+    for l in range(L):
+        lay = wl.gen_layer(w, l, args.seed)
+        cv = (lambda a: torch.from_numpy(a.view(np.int16)).view(dt).cuda()) \
+            if w.dtype == "bf16" else (lambda a: torch.from_numpy(a).cuda())
+        qs.append(cv(lay.q))
+        kks.append(cv(lay.k))
+        vs.append(cv(lay.v))
+    print(f"# inputs generated and uploaded in {time.time() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    out = torch.empty((S, w.hq, w.d), dtype=dt, device="cuda")
+    lse = torch.empty((w.hq, S), dtype=torch.float32, device="cuda")
+    evid = torch.empty((L, w.hq, T), dtype=torch.float32, device="cuda")
+    tmass = torch.empty((L, w.hq, len(nf)), dtype=torch.float32, device="cuda")
+    e_qf = torch.empty(T, dtype=torch.float32, device="cuda")
+    kk = torch.tensor(ks, dtype=torch.int32, device="cuda")
+    topk = torch.empty(max(1, sum(ks)), dtype=torch.int32, device="cuda")
+    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d), dtype=torch.uint8,
+                     device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for l in range(L):
+            ev.sparse_prefill(mask, l, L, qs[l], kks[l], vs[l], out, evid, ws,
+                              lse=lse, text_mass=tmass,
+                              softmax_scale=w.softmax_scale, stream=stream)
+        ev.frame_evidence(mask, evid, L, e_qf, k_per_seq=kk, topk=topk,
+                          stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev.profile_begin(args.steps * L)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = ev.profile_end()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    found = sorted(topk[:sum(ks)].cpu().numpy().tolist())
+    planted_ok = found == sorted(core.tolist())
+    flop_layer = 4.0 * w.block * w.block * w.d * w.hq * st["n_active_pairs"]
+    attn_ms = prof["attention_ms"] / max(1, prof["calls"])
+    achieved = flop_layer / (attn_ms * 1e-3) / 1e12
+    ev_ms = prof["evidence_ms"] / max(1, prof["calls"])
+    ev_bytes = 4.0 * w.hq * (st["n_text_rows"] * T + st["n_text_rows"] + T)
+    rec = {
+        "metric": "probe prefill tokens/sec + active-block attention TFLOP/s "
+                  "(% bf16 MFMA peak)",
+        "value": S / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) Q/K/V, planted frames)",
+        "config": {"workload": w.name, "layers": L, "tokens": S,
+                   "frames": T, "tokens_per_frame": w.tokens_per_frame,
+                   "query_tokens": int(sum(nt)), "hq": w.hq, "hkv": w.hkv,
+                   "head_dim": w.d, "block": w.block,
+                   "sink_blocks": w.sink_blocks, "window": w.window,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "mfma", "achieved": achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "attn_kernel<Bf16Path<128>>",
+                     "flop_per_launch": flop_layer,
+                     "avg_launch_ms": attn_ms},
+        "kernels_ms_per_layer": {
+            "attention": attn_ms,
+            "combine": prof["combine_ms"] / max(1, prof["calls"]),
+            "evidence": ev_ms},
+        "evidence_reduce_GBps": ev_bytes / (ev_ms * 1e-3) / 1e9,
+        "topk_planted_recovered": planted_ok,
+    }
+    if not args.no_cpu_baseline and rank == 0:
+        print("# timing the CPU oracle on one layer ...", file=sys.stderr,
+              flush=True)
+        rec["cpu_baseline"] = cpu_baseline(w, args.seed)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

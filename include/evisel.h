@@ -1,0 +1,201 @@
+/*
+ * evisel.h -- C ABI of libevisel.so, the MI355X (gfx950) sparse-prefill
+ * evidence probe.
+ *
+ * The probe runs block-sparse causal attention over a packed batch of videos
+ * laid out as X = [X_sys; X_vis; X_Q] (system prefix, N_v visual tokens per
+ * anchor frame, query tokens), and in the same pass reduces the query rows'
+ * softmax mass onto the anchor frames (the query-frame evidence cue). The
+ * layout, the frame-aligned block partition, the always-visible system prefix
+ * and the exact causal prefix of the current block follow the paper's
+ * appendix "Detailed Sparse Prefilling"; the evidence follows "Evidence
+ * Decomposition" (query-frame cue A_qf, timestamp-aligned E_qf, heads
+ * averaged per layer).
+ *
+ * Conventions for every call:
+ *  - Status codes, never exceptions. On failure nothing is launched and
+ *    evisel_last_error() returns a message (thread-local, valid until the
+ *    next failing call on the same thread).
+ *  - "device" pointers are HIP device allocations on the current device;
+ *    "host" pointers are ordinary host memory, read during the call only.
+ *    Tensors are dense, row-major, 16-byte aligned.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Kernel work is asynchronous on it; results are valid once it syncs.
+ *  - Tokens of all videos are packed: Q/O are [S, Hq, d], K/V [S, Hkv, d]
+ *    with d contiguous. Query head h reads kv head h / (Hq / Hkv).
+ */
+#ifndef EVISEL_H
+#define EVISEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EVISEL_OK = 0,
+  EVISEL_ERR_INVALID_ARG = 1, /* bad pointer, size or layout              */
+  EVISEL_ERR_UNSUPPORTED = 2, /* valid but not implemented (d, B, N_v ...) */
+  EVISEL_ERR_WORKSPACE = 3,   /* workspace missing or too small           */
+  EVISEL_ERR_HIP = 4,         /* a HIP runtime call failed                */
+  EVISEL_ERR_NOMEM = 5        /* host or device allocation failed         */
+} evisel_status;
+
+typedef enum { EVISEL_BF16 = 0, EVISEL_FP32 = 1 } evisel_dtype;
+
+/* Packed batch of videos. Video n occupies n_sys[n] + n_frames[n] * N_v +
+ * n_text[n] consecutive tokens, videos in order. Host memory, caller-owned,
+ * read during evisel_build_block_mask only. n_sys may be NULL (all zero).
+ * Requires n_seq >= 1, n_frames[n] >= 1, n_text[n] >= 1, n_sys[n] >= 0,
+ * tokens_per_frame >= 1 and fewer than 2^31 tokens in total. */
+typedef struct {
+  int32_t n_seq;
+  const int32_t* n_sys;
+  const int32_t* n_frames;
+  const int32_t* n_text;
+  int32_t tokens_per_frame; /* N_v */
+} evisel_layout;
+
+/* Static block-sparse rule (appendix: frame-aligned blocks of B tokens per
+ * region, the last block of a region may be short). A visual query token in
+ * visual block b sees visual blocks [0, sink_blocks), [b - window, b - 1]
+ * and its own block b up to itself; window = -1 makes every preceding visual
+ * block visible (plain causal attention). A query (text) token sees every
+ * visual block and the query tokens up to itself. System-prefix tokens are
+ * visible to every later token of their video. Videos never see each other. */
+typedef struct {
+  int32_t block;       /* B >= 1; the attention kernel supports B = 64 */
+  int32_t sink_blocks; /* >= 0 */
+  int32_t window;      /* >= 0, or -1 for all-causal */
+} evisel_mask_rule;
+
+typedef struct evisel_mask evisel_mask; /* opaque, library-owned */
+
+typedef struct {
+  int64_t n_tokens;        /* S                                         */
+  int64_t n_frames_total;  /* T = sum n_frames                          */
+  int64_t n_text_rows;     /* sum n_text                                */
+  int64_t n_blocks;        /* region blocks (query and key tiles)       */
+  int64_t n_active_pairs;  /* active (query block, key block) pairs     */
+  int64_t n_work_items;    /* attention work items (all heads)          */
+  int64_t n_text_tiles;    /* query-token blocks                        */
+  int64_t n_chunk_slots;   /* split query-token work items (all heads)  */
+  int32_t hq, hkv, block, tokens_per_frame;
+} evisel_mask_stats;
+
+/* Builds the block partition, the compact list of active block pairs (CSR,
+ * each row's key blocks in increasing order) and the attention work list
+ * for Hq query heads and Hkv kv heads, then uploads them to the current
+ * device with a copy on `stream` (the call waits for that copy). *out is
+ * library-owned; release it with evisel_mask_free. Errors: INVALID_ARG for
+ * a bad layout or rule or hq % hkv != 0, NOMEM, HIP. */
+evisel_status evisel_build_block_mask(const evisel_layout* layout,
+                                      const evisel_mask_rule* rule,
+                                      int32_t hq, int32_t hkv, void* stream,
+                                      evisel_mask** out);
+
+/* Same plan, host tables only (no device copy, no HIP call): for inspecting
+ * the plan on a machine without a GPU. Such a mask is rejected by the
+ * compute calls with INVALID_ARG. */
+evisel_status evisel_build_block_mask_host(const evisel_layout* layout,
+                                           const evisel_mask_rule* rule,
+                                           int32_t hq, int32_t hkv,
+                                           evisel_mask** out);
+
+/* Frees host and device memory of a mask (NULL is ignored). The caller must
+ * make sure no queued work still reads it. */
+void evisel_mask_free(evisel_mask* mask);
+
+evisel_status evisel_mask_info(const evisel_mask* mask, evisel_mask_stats* out);
+
+/* Copies the host plan into caller buffers (host memory; any may be NULL):
+ * per block (n_blocks entries) its first token, length, region (0 system,
+ * 1 visual, 2 query) and video; the CSR row_ptr (n_blocks + 1) and col
+ * (n_active_pairs) over block indices. */
+evisel_status evisel_mask_export(const evisel_mask* mask, int32_t* blk_start,
+                                 int32_t* blk_len, int32_t* blk_region,
+                                 int32_t* blk_video, int32_t* row_ptr,
+                                 int32_t* col);
+
+/* Copies the attention work list (n_work_items entries) in launch order:
+ * query block, query head, first and one-past-last CSR position of its key
+ * blocks, and split slot (-1 unless it is part of a split query-token row).
+ * Any pointer may be NULL. */
+evisel_status evisel_mask_export_work(const evisel_mask* mask, int32_t* qblock,
+                                      int32_t* head, int32_t* kb_begin,
+                                      int32_t* kb_end, int32_t* slot);
+
+/* Bytes of device workspace evisel_sparse_prefill needs for head dim d. */
+size_t evisel_sparse_prefill_workspace(const evisel_mask* mask, int32_t d);
+
+/* One layer of the probe (appendix sparse prefilling restricted to the rule
+ * above; evidence per Evidence Decomposition, query-frame cue).
+ *   q        device [S, Hq, d]   dtype
+ *   k, v     device [S, Hkv, d]  dtype
+ *   d        64 or 128; dtype EVISEL_BF16 or EVISEL_FP32
+ *   softmax_scale  logit scale, normally 1/sqrt(d)
+ *   out      device [S, Hq, d]   dtype: softmax(q k^T * scale) v over the
+ *            visible keys (fp32 accumulation; bf16 output rounded to nearest
+ *            even)
+ *   lse      device [Hq, S] fp32, natural-log log-sum-exp of each row's
+ *            scaled logits over its visible keys; may be NULL
+ *   evidence device [n_layers, Hq, T] fp32; slice [layer] is overwritten
+ *            with E[h, f] = sum over the query rows i of f's video of the
+ *            softmax mass of row i on frame f's visual tokens (a raw sum
+ *            over query rows, not a mean)
+ *   text_mass device [n_layers, Hq, n_seq] fp32 or NULL; slice [layer] gets
+ *            the same rows' mass on non-visual keys (system prefix and query
+ *            tokens); per video sum_f E + text_mass = n_text
+ *   workspace device, >= evisel_sparse_prefill_workspace(mask, d) bytes
+ * Requires B = 64, N_v dividing 64 with N_v >= 8 (when any video has
+ * query rows reducing onto frames), 0 <= layer < n_layers.
+ * Errors: INVALID_ARG (NULL buffer, host-only mask, layer out of range),
+ * UNSUPPORTED (d, dtype, B or N_v), WORKSPACE, HIP (launch failure). */
+evisel_status evisel_sparse_prefill(const evisel_mask* mask, int32_t layer,
+                                    int32_t n_layers, const void* q,
+                                    const void* k, const void* v, int32_t d,
+                                    evisel_dtype dtype, float softmax_scale,
+                                    void* out, float* lse, float* evidence,
+                                    float* text_mass, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
+/* Aggregates evidence [n_layers, Hq, T] (Evidence Decomposition: mean over
+ * heads per layer, then the timestamp-aligned query-frame score):
+ *   e_qf_layer device [n_layers, T] or NULL:
+ *              sum_h E[l, h, t] / (Hq * n_text(video of t))
+ *   e_qf       device [T]: mean over layers of e_qf_layer
+ *   k_per_seq  device [n_seq] int32, or NULL (no top-k); each value is
+ *              clamped to [0, n_frames[n]]
+ *   topk_idx   device [sum of clamped k] int32: per video, in video order,
+ *              the k local frame indices with the largest e_qf, ordered by
+ *              (e_qf descending, index ascending); NaN ranks as -inf
+ * Errors: INVALID_ARG, UNSUPPORTED (a video with more than 65536 frames
+ * when top-k is requested), HIP. */
+evisel_status evisel_frame_evidence(const evisel_mask* mask,
+                                    const float* evidence, int32_t n_layers,
+                                    float* e_qf_layer, float* e_qf,
+                                    const int32_t* k_per_seq,
+                                    int32_t* topk_idx, void* stream);
+
+/* Kernel timing, a tracing aid. evisel_profile_begin creates 4 * capacity
+ * HIP events on the current device; each later evisel_sparse_prefill call,
+ * up to `capacity` calls, records events on its stream before the attention
+ * kernel, after it, after the split-row combine and after the evidence
+ * reduction. evisel_profile_end waits for those events, writes the summed
+ * milliseconds of each kernel and the number of timed calls (any pointer may
+ * be NULL) and destroys the events. One session at a time per process; not
+ * thread-safe. Errors: INVALID_ARG (capacity < 1, a session already open or
+ * none open), NOMEM, HIP. */
+evisel_status evisel_profile_begin(int32_t capacity);
+evisel_status evisel_profile_end(double* ms_attention, double* ms_combine,
+                                 double* ms_evidence, int64_t* n_calls);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* evisel_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EVISEL_H */

@@ -1,0 +1,415 @@
+// C ABI of libevisel.so: argument validation, plan upload, launches.
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "evisel.h"
+#include "kernels.h"
+#include "plan.h"
+
+struct evisel_mask {
+  evisel::Plan plan;
+  void* dev = nullptr;  // one device allocation holding every table
+  evisel::DevPlan dp{};
+  int device = -1;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+evisel_status fail(evisel_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+evisel_status hip_fail(hipError_t e, const char* what) {
+  return fail(EVISEL_ERR_HIP,
+              std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+evisel_status make_plan(const evisel_layout* layout,
+                        const evisel_mask_rule* rule, int32_t hq, int32_t hkv,
+                        evisel_mask** out, evisel_mask** made) {
+  *made = nullptr;
+  if (!layout || !rule || !out)
+    return fail(EVISEL_ERR_INVALID_ARG, "null layout, rule or out pointer");
+  *out = nullptr;
+  if (layout->n_seq < 1 || !layout->n_frames || !layout->n_text)
+    return fail(EVISEL_ERR_INVALID_ARG,
+                "layout needs n_seq >= 1 and n_frames/n_text arrays");
+  evisel::Layout L;
+  L.Nv = layout->tokens_per_frame;
+  L.n_frames.assign(layout->n_frames, layout->n_frames + layout->n_seq);
+  L.n_text.assign(layout->n_text, layout->n_text + layout->n_seq);
+  if (layout->n_sys)
+    L.n_sys.assign(layout->n_sys, layout->n_sys + layout->n_seq);
+  evisel::Rule R;
+  R.block = rule->block;
+  R.sink = rule->sink_blocks;
+  R.window = rule->window;
+  evisel_mask* m = new (std::nothrow) evisel_mask();
+  if (!m) return fail(EVISEL_ERR_NOMEM, "host allocation failed");
+  std::string err;
+  try {
+    err = evisel::build_plan(L, R, hq, hkv, &m->plan);
+  } catch (const std::bad_alloc&) {
+    delete m;
+    return fail(EVISEL_ERR_NOMEM, "host allocation failed");
+  }
+  if (!err.empty()) {
+    delete m;
+    return fail(EVISEL_ERR_INVALID_ARG, err);
+  }
+  *made = m;
+  return EVISEL_OK;
+}
+
+template <class T>
+size_t put(std::vector<char>& buf, const std::vector<T>& v) {
+  const size_t off = align256(buf.size());
+  buf.resize(off + align256(v.size() * sizeof(T) + 1));
+  if (!v.empty()) std::memcpy(buf.data() + off, v.data(), v.size() * sizeof(T));
+  return off;
+}
+
+evisel_status upload(evisel_mask* m, hipStream_t s) {
+  const evisel::Plan& P = m->plan;
+  std::vector<char> buf;
+  const size_t o_blk = put(buf, P.blocks), o_col = put(buf, P.col),
+               o_it = put(buf, P.items), o_seq = put(buf, P.seqs),
+               o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq);
+  hipError_t e = hipGetDevice(&m->device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipMalloc(&m->dev, buf.size());
+  if (e != hipSuccess) {
+    m->dev = nullptr;
+    return e == hipErrorOutOfMemory ? fail(EVISEL_ERR_NOMEM, "hipMalloc")
+                                    : hip_fail(e, "hipMalloc");
+  }
+  e = hipMemcpyAsync(m->dev, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "plan upload");
+  char* d = (char*)m->dev;
+  evisel::DevPlan& dp = m->dp;
+  dp.blocks = (const evisel::BlockDesc*)(d + o_blk);
+  dp.col = (const int32_t*)(d + o_col);
+  dp.items = (const evisel::WorkItem*)(d + o_it);
+  dp.seqs = (const evisel::SeqDesc*)(d + o_seq);
+  dp.tiles = (const evisel::TextTile*)(d + o_tt);
+  dp.frame_seq = (const int32_t*)(d + o_fs);
+  dp.n_items = (int32_t)P.items.size();
+  dp.n_tiles = (int32_t)P.tiles.size();
+  dp.n_seq = (int32_t)P.seqs.size();
+  dp.S = (int32_t)P.S;
+  dp.T = (int32_t)P.T;
+  dp.n_text_rows = (int32_t)P.n_text_rows;
+  dp.segtot = P.segtot;
+  dp.hq = P.hq;
+  dp.hkv = P.hkv;
+  dp.Nv = P.layout.Nv;
+  return EVISEL_OK;
+}
+
+struct WsLayout {
+  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, total;
+};
+
+WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
+  WsLayout w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t rows = (size_t)P.n_slots * 64;
+  w.pO = take(rows * d * 4);
+  w.pM = take(rows * 4);
+  w.pL = take(rows * 4);
+  w.pNV = take(rows * 4);
+  w.seg = take((size_t)P.hq * P.segtot * 4);
+  w.lse2t = take((size_t)P.hq * P.n_text_rows * 4);
+  w.tmpart = take((size_t)P.hq * P.tiles.size() * 4);
+  w.total = off;
+  return w;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Kernel timing session (evisel_profile_begin / _end).
+struct Profile {
+  bool open = false;
+  std::vector<hipEvent_t> ev;  // 4 per timed call
+  size_t used = 0;             // calls recorded
+};
+Profile g_prof;
+
+void prof_record(size_t call, int k, hipStream_t s) {
+  (void)hipEventRecord(g_prof.ev[4 * call + k], s);
+}
+
+evisel_status check_device(const evisel_mask* m) {
+  if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
+  if (!m->dev)
+    return fail(EVISEL_ERR_INVALID_ARG,
+                "mask has no device copy (built with _host)");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != m->device)
+    return fail(EVISEL_ERR_INVALID_ARG,
+                "current device differs from the mask's device");
+  return EVISEL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+evisel_status evisel_build_block_mask(const evisel_layout* layout,
+                                      const evisel_mask_rule* rule, int32_t hq,
+                                      int32_t hkv, void* stream,
+                                      evisel_mask** out) {
+  evisel_mask* m = nullptr;
+  evisel_status st = make_plan(layout, rule, hq, hkv, out, &m);
+  if (st != EVISEL_OK) return st;
+  st = upload(m, (hipStream_t)stream);
+  if (st != EVISEL_OK) {
+    evisel_mask_free(m);
+    return st;
+  }
+  *out = m;
+  return EVISEL_OK;
+}
+
+evisel_status evisel_build_block_mask_host(const evisel_layout* layout,
+                                           const evisel_mask_rule* rule,
+                                           int32_t hq, int32_t hkv,
+                                           evisel_mask** out) {
+  evisel_mask* m = nullptr;
+  evisel_status st = make_plan(layout, rule, hq, hkv, out, &m);
+  if (st != EVISEL_OK) return st;
+  *out = m;
+  return EVISEL_OK;
+}
+
+void evisel_mask_free(evisel_mask* mask) {
+  if (!mask) return;
+  if (mask->dev) (void)hipFree(mask->dev);
+  delete mask;
+}
+
+evisel_status evisel_mask_info(const evisel_mask* m, evisel_mask_stats* out) {
+  if (!m || !out) return fail(EVISEL_ERR_INVALID_ARG, "null argument");
+  const evisel::Plan& P = m->plan;
+  out->n_tokens = P.S;
+  out->n_frames_total = P.T;
+  out->n_text_rows = P.n_text_rows;
+  out->n_blocks = (int64_t)P.blocks.size();
+  out->n_active_pairs = (int64_t)P.col.size();
+  out->n_work_items = (int64_t)P.items.size();
+  out->n_text_tiles = (int64_t)P.tiles.size();
+  out->n_chunk_slots = P.n_slots;
+  out->hq = P.hq;
+  out->hkv = P.hkv;
+  out->block = P.rule.block;
+  out->tokens_per_frame = P.layout.Nv;
+  return EVISEL_OK;
+}
+
+evisel_status evisel_mask_export(const evisel_mask* m, int32_t* blk_start,
+                                 int32_t* blk_len, int32_t* blk_region,
+                                 int32_t* blk_video, int32_t* row_ptr,
+                                 int32_t* col) {
+  if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
+  const evisel::Plan& P = m->plan;
+  for (size_t b = 0; b < P.blocks.size(); ++b) {
+    if (blk_start) blk_start[b] = P.blocks[b].start;
+    if (blk_len) blk_len[b] = P.blocks[b].len;
+    if (blk_region) blk_region[b] = P.blocks[b].region;
+  }
+  if (blk_video) {
+    size_t b = 0;
+    for (size_t n = 0; n < P.seqs.size(); ++n)
+      while (b < P.blocks.size() && P.blocks[b].start < P.seqs[n].end)
+        blk_video[b++] = (int32_t)n;
+  }
+  if (row_ptr)
+    std::memcpy(row_ptr, P.row_ptr.data(), P.row_ptr.size() * 4);
+  if (col && !P.col.empty()) std::memcpy(col, P.col.data(), P.col.size() * 4);
+  return EVISEL_OK;
+}
+
+evisel_status evisel_mask_export_work(const evisel_mask* m, int32_t* qblock,
+                                      int32_t* head, int32_t* kb_begin,
+                                      int32_t* kb_end, int32_t* slot) {
+  if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
+  const auto& it = m->plan.items;
+  for (size_t i = 0; i < it.size(); ++i) {
+    if (qblock) qblock[i] = it[i].qblock;
+    if (head) head[i] = it[i].head;
+    if (kb_begin) kb_begin[i] = it[i].kb_begin;
+    if (kb_end) kb_end[i] = it[i].kb_end;
+    if (slot) slot[i] = it[i].slot;
+  }
+  return EVISEL_OK;
+}
+
+size_t evisel_sparse_prefill_workspace(const evisel_mask* m, int32_t d) {
+  if (!m || (d != 64 && d != 128)) return 0;
+  return ws_layout(m->plan, d).total;
+}
+
+evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
+                                    int32_t n_layers, const void* q,
+                                    const void* k, const void* v, int32_t d,
+                                    evisel_dtype dtype, float softmax_scale,
+                                    void* out, float* lse, float* evidence,
+                                    float* text_mass, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  const evisel::Plan& P = m->plan;
+  if (n_layers < 1 || layer < 0 || layer >= n_layers)
+    return fail(EVISEL_ERR_INVALID_ARG, "need 0 <= layer < n_layers");
+  if (!q || !k || !v || !out || !evidence)
+    return fail(EVISEL_ERR_INVALID_ARG, "null q, k, v, out or evidence");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(EVISEL_ERR_INVALID_ARG, "q, k, v, out must be 16-byte aligned");
+  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
+    return fail(EVISEL_ERR_INVALID_ARG, "softmax_scale must be positive");
+  if (d != 64 && d != 128)
+    return fail(EVISEL_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  if (dtype != EVISEL_BF16 && dtype != EVISEL_FP32)
+    return fail(EVISEL_ERR_UNSUPPORTED, "dtype must be bf16 or fp32");
+  if (P.rule.block != 64)
+    return fail(EVISEL_ERR_UNSUPPORTED, "attention kernel needs block = 64");
+  const int nv = P.layout.Nv;
+  if (nv < 8 || 64 % nv != 0)
+    return fail(EVISEL_ERR_UNSUPPORTED,
+                "tokens_per_frame must divide 64 and be >= 8");
+  const WsLayout wl = ws_layout(P, d);
+  if (!workspace || workspace_bytes < wl.total)
+    return fail(EVISEL_ERR_WORKSPACE,
+                "workspace needs " + std::to_string(wl.total) + " bytes");
+  if ((uintptr_t)workspace & 255)
+    return fail(EVISEL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  char* wb = (char*)workspace;
+  evisel::Workspace w;
+  w.pO = (float*)(wb + wl.pO);
+  w.pM = (float*)(wb + wl.pM);
+  w.pL = (float*)(wb + wl.pL);
+  w.pNV = (float*)(wb + wl.pNV);
+  w.seg = (float*)(wb + wl.seg);
+  w.lse2t = (float*)(wb + wl.lse2t);
+  w.tmpart = (float*)(wb + wl.tmpart);
+  evisel::AttnCall c;
+  c.q = q;
+  c.k = k;
+  c.v = v;
+  c.o = out;
+  c.lse = lse;
+  c.scale_log2 = softmax_scale * 1.4426950408889634f;
+  c.d = d;
+  c.fp32 = dtype == EVISEL_FP32;
+  hipStream_t s = (hipStream_t)stream;
+  const bool prof = g_prof.open && g_prof.used < g_prof.ev.size() / 4;
+  const size_t call = g_prof.used;
+  if (prof) prof_record(call, 0, s);
+  hipError_t e = evisel::launch_attention(m->dp, w, c, s);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  if (prof) prof_record(call, 1, s);
+  e = evisel::launch_combine(m->dp, w, c, s);
+  if (e != hipSuccess) return hip_fail(e, "combine launch");
+  if (prof) prof_record(call, 2, s);
+  e = evisel::launch_evidence(
+      m->dp, w, evidence + (size_t)layer * P.hq * P.T,
+      text_mass ? text_mass + (size_t)layer * P.hq * P.seqs.size() : nullptr,
+      s);
+  if (e != hipSuccess) return hip_fail(e, "evidence launch");
+  if (prof) {
+    prof_record(call, 3, s);
+    g_prof.used++;
+  }
+  return EVISEL_OK;
+}
+
+evisel_status evisel_frame_evidence(const evisel_mask* m,
+                                    const float* evidence, int32_t n_layers,
+                                    float* e_qf_layer, float* e_qf,
+                                    const int32_t* k_per_seq,
+                                    int32_t* topk_idx, void* stream) {
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  if (!evidence || !e_qf || n_layers < 1)
+    return fail(EVISEL_ERR_INVALID_ARG, "null evidence/e_qf or n_layers < 1");
+  if (k_per_seq && !topk_idx)
+    return fail(EVISEL_ERR_INVALID_ARG, "k_per_seq given without topk_idx");
+  if (k_per_seq)
+    for (const auto& sq : m->plan.seqs)
+      if (sq.n_frames > 65536)
+        return fail(EVISEL_ERR_UNSUPPORTED,
+                    "top-k supports at most 65536 frames per video");
+  hipError_t e = evisel::launch_frame_evidence(m->dp, evidence, n_layers,
+                                               e_qf_layer, e_qf, k_per_seq,
+                                               topk_idx, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "frame evidence launch");
+  return EVISEL_OK;
+}
+
+evisel_status evisel_profile_begin(int32_t capacity) {
+  if (capacity < 1) return fail(EVISEL_ERR_INVALID_ARG, "capacity < 1");
+  if (g_prof.open)
+    return fail(EVISEL_ERR_INVALID_ARG, "a profiling session is open");
+  g_prof = Profile();
+  try {
+    g_prof.ev.resize((size_t)capacity * 4);
+  } catch (const std::bad_alloc&) {
+    return fail(EVISEL_ERR_NOMEM, "host allocation failed");
+  }
+  for (size_t i = 0; i < g_prof.ev.size(); ++i) {
+    hipError_t e = hipEventCreate(&g_prof.ev[i]);
+    if (e != hipSuccess) {
+      for (size_t j = 0; j < i; ++j) (void)hipEventDestroy(g_prof.ev[j]);
+      g_prof = Profile();
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  g_prof.open = true;
+  return EVISEL_OK;
+}
+
+evisel_status evisel_profile_end(double* ms_attention, double* ms_combine,
+                                 double* ms_evidence, int64_t* n_calls) {
+  if (!g_prof.open)
+    return fail(EVISEL_ERR_INVALID_ARG, "no profiling session is open");
+  double ms[3] = {0, 0, 0};
+  hipError_t err = hipSuccess;
+  for (size_t c = 0; c < g_prof.used && err == hipSuccess; ++c) {
+    err = hipEventSynchronize(g_prof.ev[4 * c + 3]);
+    for (int k = 0; k < 3 && err == hipSuccess; ++k) {
+      float t = 0.f;
+      err = hipEventElapsedTime(&t, g_prof.ev[4 * c + k],
+                                g_prof.ev[4 * c + k + 1]);
+      ms[k] += t;
+    }
+  }
+  const int64_t used = (int64_t)g_prof.used;
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof = Profile();
+  if (err != hipSuccess) return hip_fail(err, "profile events");
+  if (ms_attention) *ms_attention = ms[0];
+  if (ms_combine) *ms_combine = ms[1];
+  if (ms_evidence) *ms_evidence = ms[2];
+  if (n_calls) *n_calls = used;
+  return EVISEL_OK;
+}
+
+const char* evisel_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

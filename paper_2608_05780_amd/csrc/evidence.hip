@@ -1,0 +1,127 @@
+// Evidence reduction and frame aggregation (gfx950).
+//
+// evidence_kernel: E[h, f] = sum over the query rows r of f's video of
+//   exp2(seg[h, r, f] - lse2[h, r]), i.e. each row's softmax mass on frame f
+//   (the query-frame cue of Evidence Decomposition, kept as a raw sum over the
+//   query rows). One thread per (head, frame), rows in a fixed order, one
+//   store per output: no atomics, bitwise reproducible. Adjacent threads read
+//   adjacent frames of the same row, so every load is coalesced.
+// frame_mean_kernel: E_qf[l, t] = sum_h E[l, h, t] / (Hq * n_text) and the
+//   mean over layers (heads averaged per layer, layer kept).
+// topk_kernel: per video, rank r(t) = #{t' : e(t') > e(t) or (e(t') == e(t)
+//   and t' < t)}; frames with r(t) < k land at topk[offset + r(t)]. Ranks of a
+//   strict total order are a permutation, so every slot gets one writer.
+#include "kernels.h"
+
+namespace evisel {
+namespace {
+
+__device__ __forceinline__ float exp2_(float x) {
+  return __builtin_amdgcn_exp2f(x);
+}
+
+__global__ __launch_bounds__(256) void evidence_kernel(const DevPlan pl,
+                                                       const Workspace ws,
+                                                       float* __restrict__ ev,
+                                                       float* __restrict__ tm) {
+  const int h = blockIdx.y;
+  const int f = blockIdx.x * 256 + threadIdx.x;
+  if (f < pl.T) {
+    const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
+    const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
+                       (f - sq.frame0);
+    const float* l2 = ws.lse2t + (size_t)h * pl.n_text_rows + sq.textrow0;
+    float acc = 0.f;
+    for (int r = 0; r < sq.n_text; ++r)
+      acc += exp2_(src[(size_t)r * sq.n_frames] - l2[r]);
+    ev[(size_t)h * pl.T + f] = acc;
+  }
+  if (tm && blockIdx.x == 0) {
+    for (int n = threadIdx.x; n < pl.n_seq; n += 256) {
+      const SeqDesc sq = pl.seqs[n];
+      float t = 0.f;
+      for (int i = 0; i < sq.n_tiles; ++i)
+        t += ws.tmpart[(size_t)h * pl.n_tiles + sq.tile0 + i];
+      tm[(size_t)h * pl.n_seq + n] = t;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void frame_mean_kernel(
+    const DevPlan pl, const float* __restrict__ ev, int n_layers,
+    float* __restrict__ e_layer, float* __restrict__ e_qf) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= pl.T) return;
+  const SeqDesc sq = pl.seqs[pl.frame_seq[t]];
+  const float denom = (float)pl.hq * (float)sq.n_text;
+  float pooled = 0.f;
+  for (int l = 0; l < n_layers; ++l) {
+    float s = 0.f;
+    for (int h = 0; h < pl.hq; ++h)
+      s += ev[((size_t)l * pl.hq + h) * pl.T + t];
+    const float v = s / denom;
+    if (e_layer) e_layer[(size_t)l * pl.T + t] = v;
+    pooled += v;
+  }
+  e_qf[t] = pooled / (float)n_layers;
+}
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkLds = 16384;   // frames held in LDS per video
+
+__device__ __forceinline__ float rank_key(float x) {
+  return x != x ? -__builtin_inff() : x;   // NaN ranks like -inf
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(
+    const DevPlan pl, const float* __restrict__ e_qf,
+    const int* __restrict__ kps, int* __restrict__ topk) {
+  __shared__ float vals[kTopkLds];
+  const int n = blockIdx.x;
+  const SeqDesc sq = pl.seqs[n];
+  const int F = sq.n_frames;
+  int off = 0;
+  for (int i = 0; i < n; ++i) off += min(max(kps[i], 0), pl.seqs[i].n_frames);
+  const int k = min(max(kps[n], 0), F);
+  if (k == 0) return;
+  const float* src = e_qf + sq.frame0;
+  const bool in_lds = F <= kTopkLds;
+  if (in_lds) {
+    for (int t = threadIdx.x; t < F; t += kTopkThreads)
+      vals[t] = rank_key(src[t]);
+    __syncthreads();
+  }
+  for (int t = threadIdx.x; t < F; t += kTopkThreads) {
+    const float v = in_lds ? vals[t] : rank_key(src[t]);
+    int rank = 0;
+    for (int u = 0; u < F; ++u) {
+      const float w = in_lds ? vals[u] : rank_key(src[u]);
+      rank += (w > v) || (w == v && u < t);
+    }
+    if (rank < k) topk[off + rank] = t;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_evidence(const DevPlan& p, const Workspace& w, float* ev,
+                           float* tm, hipStream_t s) {
+  dim3 grid((p.T + 255) / 256, p.hq), block(256);
+  evidence_kernel<<<grid, block, 0, s>>>(p, w, ev, tm);
+  return hipGetLastError();
+}
+
+hipError_t launch_frame_evidence(const DevPlan& p, const float* evidence,
+                                 int32_t n_layers, float* e_qf_layer,
+                                 float* e_qf, const int32_t* k_per_seq,
+                                 int32_t* topk, hipStream_t s) {
+  frame_mean_kernel<<<dim3((p.T + 255) / 256), dim3(256), 0, s>>>(
+      p, evidence, n_layers, e_qf_layer, e_qf);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !k_per_seq) return e;
+  topk_kernel<<<dim3(p.n_seq), dim3(kTopkThreads), 0, s>>>(p, e_qf, k_per_seq,
+                                                           topk);
+  return hipGetLastError();
+}
+
+}  // namespace evisel

@@ -1,0 +1,57 @@
+// Kernel launchers (defined in attn.hip and evidence.hip, called from api.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "plan.h"
+
+namespace evisel {
+
+// Device views of the plan tables (one allocation, owned by the mask).
+struct DevPlan {
+  const BlockDesc* blocks;
+  const int32_t* col;
+  const WorkItem* items;
+  const SeqDesc* seqs;
+  const TextTile* tiles;
+  const int32_t* frame_seq;
+  int32_t n_items, n_tiles, n_seq;
+  int32_t S, T, n_text_rows;
+  int64_t segtot;
+  int32_t hq, hkv, Nv;
+};
+
+// Workspace carve-up for one prefill call.
+struct Workspace {
+  float* pO;     // [slots][64][d]  unnormalised partial outputs
+  float* pM;     // [slots][64]     reference max (log2 units)
+  float* pL;     // [slots][64]     partial row sums
+  float* pNV;    // [slots][64]     log2 partial mass on non-visual keys
+  float* seg;    // [hq][segtot]    log2 partial mass per (query row, frame)
+  float* lse2t;  // [hq][n_text_rows] log2 LSE of query rows
+  float* tmpart; // [hq][n_tiles]   non-visual mass per query tile
+};
+
+struct AttnCall {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;            // may be null
+  float scale_log2;      // softmax scale * log2(e)
+  int32_t d;
+  int32_t fp32;          // 1: fp32 inputs/outputs, 0: bf16
+};
+
+hipError_t launch_attention(const DevPlan& p, const Workspace& w,
+                            const AttnCall& c, hipStream_t s);
+hipError_t launch_combine(const DevPlan& p, const Workspace& w,
+                          const AttnCall& c, hipStream_t s);
+hipError_t launch_evidence(const DevPlan& p, const Workspace& w,
+                           float* evidence_layer, float* text_mass_layer,
+                           hipStream_t s);
+hipError_t launch_frame_evidence(const DevPlan& p, const float* evidence,
+                                 int32_t n_layers, float* e_qf_layer,
+                                 float* e_qf, const int32_t* k_per_seq,
+                                 int32_t* topk, hipStream_t s);
+
+}  // namespace evisel

@@ -1,0 +1,230 @@
+// Host plan builder: block partition, active block pairs, work list.
+//
+// Blocks follow the frame-aligned partition of the paper's appendix
+// ("Detailed Sparse Prefilling"): every region of every video (system prefix,
+// visual tokens, query tokens) is cut into blocks of B tokens from the
+// region's start, the last one possibly short, and no block crosses a video.
+// Active pairs follow the static rule of evisel_mask_rule: the system prefix
+// is always visible, a visual block keeps the sink blocks, `window` preceding
+// blocks and itself, a query-token block keeps every visual block and the
+// query-token blocks up to itself.
+#include "plan.h"
+
+#include <algorithm>
+#include <numeric>
+
+namespace evisel {
+namespace {
+
+struct Item {
+  WorkItem w;
+  int64_t cost;
+};
+
+}  // namespace
+
+std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
+                       Plan* out) {
+  const size_t nseq = L.n_frames.size();
+  if (nseq == 0) return "layout has no video";
+  if (L.n_text.size() != nseq || (!L.n_sys.empty() && L.n_sys.size() != nseq))
+    return "layout arrays differ in length";
+  if (L.Nv < 1) return "tokens_per_frame must be >= 1";
+  if (R.block < 1) return "block must be >= 1";
+  if (R.sink < 0) return "sink_blocks must be >= 0";
+  if (R.window < -1) return "window must be >= 0 or -1";
+  if (hq < 1 || hkv < 1 || hq % hkv != 0)
+    return "head counts must satisfy hq >= 1, hkv >= 1, hq % hkv == 0";
+  if (hq > 4096) return "hq too large";
+
+  Plan& P = *out;
+  P = Plan();
+  P.layout = L;
+  if (P.layout.n_sys.empty()) P.layout.n_sys.assign(nseq, 0);
+  P.rule = R;
+  P.hq = hq;
+  P.hkv = hkv;
+
+  // ---- videos and blocks -------------------------------------------------
+  int64_t tok = 0, frame = 0, trow = 0, segbase = 0;
+  std::vector<std::vector<int32_t>> sysb(nseq), visb(nseq), txtb(nseq);
+  for (size_t n = 0; n < nseq; ++n) {
+    const int64_t ns = P.layout.n_sys[n], nf = L.n_frames[n], nt = L.n_text[n];
+    if (ns < 0 || nf < 1 || nt < 1)
+      return "video " + std::to_string(n) +
+             ": need n_sys >= 0, n_frames >= 1, n_text >= 1";
+    const int64_t nvis = nf * L.Nv;
+    SeqDesc s{};
+    s.tok0 = (int32_t)tok;
+    s.vis0 = (int32_t)(tok + ns);
+    s.txt0 = (int32_t)(tok + ns + nvis);
+    const int64_t end = tok + ns + nvis + nt;
+    if (end >= (int64_t(1) << 31) - 64) return "too many tokens (>= 2^31)";
+    s.end = (int32_t)end;
+    s.frame0 = (int32_t)frame;
+    s.n_frames = (int32_t)nf;
+    s.textrow0 = (int32_t)trow;
+    s.n_text = (int32_t)nt;
+    s.segbase = segbase;
+    auto cut = [&](int64_t a, int64_t e, int32_t reg,
+                   std::vector<int32_t>& ids) {
+      for (int64_t b = a; b < e; b += R.block) {
+        BlockDesc d{};
+        d.start = (int32_t)b;
+        d.len = (int32_t)std::min<int64_t>(R.block, e - b);
+        d.region = reg;
+        d.aux = reg == kVis   ? (int32_t)(frame + (b - s.vis0) / L.Nv)
+                : reg == kTxt ? (int32_t)(trow + (b - s.txt0))
+                              : -1;
+        ids.push_back((int32_t)P.blocks.size());
+        P.blocks.push_back(d);
+      }
+    };
+    cut(s.tok0, s.vis0, kSys, sysb[n]);
+    cut(s.vis0, s.txt0, kVis, visb[n]);
+    cut(s.txt0, s.end, kTxt, txtb[n]);
+    P.seqs.push_back(s);
+    for (int64_t f = 0; f < nf; ++f) P.frame_seq.push_back((int32_t)n);
+    tok = end;
+    frame += nf;
+    trow += nt;
+    segbase += nt * nf;
+  }
+  P.S = tok;
+  P.T = frame;
+  P.n_text_rows = trow;
+  P.segtot = segbase;
+
+  // ---- CSR of active pairs ----------------------------------------------
+  const int32_t nb = (int32_t)P.blocks.size();
+  P.row_ptr.assign(nb + 1, 0);
+  std::vector<int32_t> rowlist;
+  for (size_t n = 0; n < nseq; ++n) {
+    const auto &sb = sysb[n], &vb = visb[n], &tb = txtb[n];
+    for (size_t j = 0; j < sb.size(); ++j) {   // system rows: causal prefix
+      rowlist.assign(sb.begin(), sb.begin() + j + 1);
+      P.row_ptr[sb[j] + 1] = (int32_t)rowlist.size();
+      P.col.insert(P.col.end(), rowlist.begin(), rowlist.end());
+    }
+    const int32_t nvb = (int32_t)vb.size();
+    for (int32_t i = 0; i < nvb; ++i) {        // visual rows
+      rowlist.assign(sb.begin(), sb.end());
+      const int32_t lo = R.window < 0 ? 0 : std::max(0, i - R.window);
+      for (int32_t b = 0; b < std::min(R.sink, lo); ++b)
+        rowlist.push_back(vb[b]);
+      for (int32_t b = lo; b <= i; ++b) rowlist.push_back(vb[b]);
+      P.row_ptr[vb[i] + 1] = (int32_t)rowlist.size();
+      P.col.insert(P.col.end(), rowlist.begin(), rowlist.end());
+    }
+    for (size_t t = 0; t < tb.size(); ++t) {   // query-token rows: dense
+      rowlist.assign(sb.begin(), sb.end());
+      rowlist.insert(rowlist.end(), vb.begin(), vb.end());
+      rowlist.insert(rowlist.end(), tb.begin(), tb.begin() + t + 1);
+      P.row_ptr[tb[t] + 1] = (int32_t)rowlist.size();
+      P.col.insert(P.col.end(), rowlist.begin(), rowlist.end());
+    }
+  }
+  // row_ptr currently holds row lengths at [b+1]; blocks are numbered in
+  // token order and rows were appended in the same order, so a prefix sum
+  // gives the offsets.
+  for (int32_t b = 0; b < nb; ++b) P.row_ptr[b + 1] += P.row_ptr[b];
+  if ((int64_t)P.row_ptr[nb] != (int64_t)P.col.size())
+    return "internal error: CSR size mismatch";
+
+  // ---- work items ---------------------------------------------------------
+  int64_t total = 0;
+  for (int32_t b = 0; b < nb; ++b)
+    total += (int64_t)(P.row_ptr[b + 1] - P.row_ptr[b]) * hq;
+  const int64_t avg = (total + kTargetSlots - 1) / kTargetSlots;
+  P.chunk_blocks = (int32_t)std::max<int64_t>(16, avg);
+
+  std::vector<Item> txt_items, other_items;
+  for (size_t n = 0; n < nseq; ++n) {
+    for (int32_t b : txtb[n]) {
+      const int32_t rb = P.row_ptr[b], re = P.row_ptr[b + 1];
+      const int32_t len = re - rb;
+      const int32_t nch = (len + P.chunk_blocks - 1) / P.chunk_blocks;
+      TextTile tt{b, (int32_t)n, nch, (int32_t)P.n_slots};
+      if (P.seqs[n].n_tiles == 0) P.seqs[n].tile0 = (int32_t)P.tiles.size();
+      P.seqs[n].n_tiles++;
+      P.tiles.push_back(tt);
+      for (int32_t h = 0; h < hq; ++h)
+        for (int32_t c = 0; c < nch; ++c) {
+          // equal-size chunks: chunk c covers [rb + c*len/nch, ...)
+          const int32_t a = rb + (int32_t)((int64_t)c * len / nch);
+          const int32_t e = rb + (int32_t)((int64_t)(c + 1) * len / nch);
+          WorkItem w{b, h, a, e, tt.slot0 + h * nch + c, (int32_t)n, c, 0};
+          txt_items.push_back({w, e - a});
+        }
+      P.n_slots += (int64_t)hq * nch;
+    }
+    // visual and system rows, ordered by (kv head, block, head) so that
+    // neighbouring launches share key/value tiles
+    const int32_t group = hq / hkv;
+    for (int32_t g = 0; g < hkv; ++g) {
+      auto add = [&](const std::vector<int32_t>& ids) {
+        for (int32_t b : ids)
+          for (int32_t hh = 0; hh < group; ++hh) {
+            const int32_t h = g * group + hh;
+            WorkItem w{b, h, P.row_ptr[b], P.row_ptr[b + 1], -1, (int32_t)n,
+                       0, 0};
+            other_items.push_back({w, P.row_ptr[b + 1] - P.row_ptr[b]});
+          }
+      };
+      add(sysb[n]);
+      add(visb[n]);
+    }
+  }
+
+  // Longest-first over the XCD queues: split query-token items go first, by
+  // LPT; the remaining items keep their locality order and are cut into
+  // contiguous runs that level the queues.
+  std::stable_sort(txt_items.begin(), txt_items.end(),
+                   [](const Item& a, const Item& b) { return a.cost > b.cost; });
+  std::vector<std::vector<WorkItem>> q(kXcds);
+  std::vector<int64_t> load(kXcds, 0);
+  for (const Item& it : txt_items) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) -
+                        load.begin());
+    q[x].push_back(it.w);
+    load[x] += it.cost + 1;
+  }
+  int64_t rest = 0;
+  for (const Item& it : other_items) rest += it.cost + 1;
+  const int64_t all = rest + std::accumulate(load.begin(), load.end(),
+                                             int64_t(0));
+  const int64_t target = (all + kXcds - 1) / kXcds;
+  size_t pos = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    while (pos < other_items.size() &&
+           (x == kXcds - 1 || load[x] + other_items[pos].cost + 1 <= target)) {
+      q[x].push_back(other_items[pos].w);
+      load[x] += other_items[pos].cost + 1;
+      ++pos;
+    }
+  }
+  // longest first inside each queue (stable: locality order kept per cost)
+  for (int x = 0; x < kXcds; ++x) {
+    std::stable_sort(q[x].begin(), q[x].end(),
+                     [](const WorkItem& a, const WorkItem& b) {
+                       return (a.kb_end - a.kb_begin) > (b.kb_end - b.kb_begin);
+                     });
+  }
+  size_t rounds = 0;
+  for (auto& v : q) rounds = std::max(rounds, v.size());
+  P.items.reserve(rounds * kXcds);
+  for (size_t r = 0; r < rounds; ++r)
+    for (int x = 0; x < kXcds; ++x) {
+      if (r < q[x].size()) {
+        P.items.push_back(q[x][r]);
+      } else {
+        WorkItem pad{-1, 0, 0, 0, -1, 0, 0, 0};
+        P.items.push_back(pad);
+      }
+    }
+  // drop trailing padding
+  while (!P.items.empty() && P.items.back().qblock < 0) P.items.pop_back();
+  return "";
+}
+
+}  // namespace evisel

@@ -1,0 +1,92 @@
+// Plan tables shared by the host builder (plan.cpp) and the HIP kernels.
+//
+// The plan is everything about a probe that depends only on the token layout,
+// the sparse rule and the head counts: the region-relative block partition,
+// the CSR of active (query block, key block) pairs, the attention work list in
+// launch order, and the bookkeeping the evidence kernels need. It is built
+// once on the host and uploaded as one device allocation.
+#pragma once
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace evisel {
+
+enum Region : int32_t { kSys = 0, kVis = 1, kTxt = 2 };
+
+// One region block: a query tile and a key tile at the same time.
+struct BlockDesc {
+  int32_t start;   // first token (global, packed)
+  int32_t len;     // 1..B tokens
+  int32_t region;  // Region
+  int32_t aux;     // visual: global frame id of its first token;
+                   // query: global query-row id of its first token; else -1
+};
+
+// Per video.
+struct SeqDesc {
+  int32_t tok0, vis0, txt0, end;        // token offsets
+  int32_t frame0, n_frames;             // global frame range
+  int32_t textrow0, n_text;             // global query-row range
+  int64_t segbase;                      // offset of the [n_text][n_frames]
+                                        // partial-LSE block (per head)
+  int32_t tile0, n_tiles;               // query-token tiles (TextTile index)
+};
+
+// One attention work item: a query block, one query head, a contiguous run
+// of that block's CSR row. Items of split query-token rows carry a slot.
+struct WorkItem {
+  int32_t qblock;    // -1: padding, exits immediately
+  int32_t head;
+  int32_t kb_begin;  // CSR positions [kb_begin, kb_end)
+  int32_t kb_end;
+  int32_t slot;      // -1 for visual/system rows; else partial-result slot
+  int32_t seq;       // video of the query block
+  int32_t chunk;     // chunk index within its row (query-token rows)
+  int32_t pad;
+};
+
+// A query-token block and its chunk slots: slot(h, c) = slot0 + h*n_chunks + c.
+struct TextTile {
+  int32_t qblock;
+  int32_t seq;
+  int32_t n_chunks;
+  int32_t slot0;
+};
+
+struct Layout {
+  std::vector<int32_t> n_sys, n_frames, n_text;
+  int32_t Nv = 0;
+};
+
+struct Rule {
+  int32_t block = 64, sink = 1, window = -1;
+};
+
+struct Plan {
+  // inputs
+  Layout layout;
+  Rule rule;
+  int32_t hq = 0, hkv = 0;
+  // sizes
+  int64_t S = 0, T = 0, n_text_rows = 0, segtot = 0, n_slots = 0;
+  int32_t chunk_blocks = 0;   // max key blocks per split item
+  // tables
+  std::vector<BlockDesc> blocks;
+  std::vector<int32_t> row_ptr, col;
+  std::vector<WorkItem> items;      // launch order
+  std::vector<SeqDesc> seqs;
+  std::vector<TextTile> tiles;
+  std::vector<int32_t> frame_seq;   // [T] video of each global frame
+};
+
+// Builds the plan; returns "" on success or an error message.
+std::string build_plan(const Layout& layout, const Rule& rule, int32_t hq,
+                       int32_t hkv, Plan* out);
+
+// Number of hardware queues the launch order interleaves (one per XCD).
+constexpr int kXcds = 8;
+// Concurrent work-item slots the split heuristic aims to fill.
+constexpr int kTargetSlots = 1024;
+
+}  // namespace evisel

@@ -1,0 +1,110 @@
+"""Runs the HIP probe through the C ABI and the oracle on the same seeded
+inputs (shared by the GPU tests, smoke() and the benchmark's checks)."""
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass
+
+import numpy as np
+
+import workloads as wl
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@dataclass
+class GpuRun:
+    O: list          # per layer numpy [S, Hq, d] float32
+    LSE: list        # per layer numpy [Hq, S]
+    E: np.ndarray    # [L, Hq, T]
+    text_mass: np.ndarray
+    e_qf: np.ndarray
+    e_qf_layer: np.ndarray
+    topk: list       # per video int arrays (local frame ids)
+    mask: object
+
+
+def to_device(layer: wl.Layer, w: wl.Workload, torch):
+    if w.dtype == "bf16":
+        cv = lambda a: torch.from_numpy(a.view(np.int16)).view(
+            torch.bfloat16).cuda()
+    else:
+        cv = lambda a: torch.from_numpy(a).cuda()
+    return cv(layer.q), cv(layer.k), cv(layer.v)
+
+
+def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
+            keep_o=True, layer_inputs=None, on_layer=None):
+    """Run ``layers`` (list of layer ids) of workload ``w`` on the GPU.
+
+    ``on_layer(j, layer_id, out, lse)`` (torch tensors on the GPU) is called
+    after each layer; with ``keep_o`` the outputs are also copied to host."""
+    import torch
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
+                               w.sink_blocks, w.window, w.hq, w.hkv,
+                               n_sys=ns)
+    st = mask.stats
+    S, T, nseq = st["n_tokens"], st["n_frames_total"], len(nf)
+    L = len(layers)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    out = torch.empty((S, w.hq, w.d), dtype=dt, device="cuda")
+    lse = torch.empty((w.hq, S), dtype=torch.float32, device="cuda")
+    evid = torch.full((L, w.hq, T), float("nan"), device="cuda")
+    tm = torch.full((L, w.hq, nseq), float("nan"), device="cuda")
+    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d), dtype=torch.uint8,
+                     device="cuda")
+    Os, LSEs = [], []
+    for j, l in enumerate(layers):
+        lay = layer_inputs(l) if layer_inputs else wl.gen_layer(w, l, seed)
+        q, k, v = to_device(lay, w, torch)
+        say(f"  gpu: {w.name} layer {l} S={S} hq={w.hq} d={w.d}")
+        ev.sparse_prefill(mask, j, L, q, k, v, out, evid, ws, lse=lse,
+                          text_mass=tm, softmax_scale=w.softmax_scale)
+        torch.cuda.synchronize()
+        if on_layer is not None:
+            on_layer(j, l, out, lse)
+        if keep_o:
+            Os.append(out.float().cpu().numpy())
+            LSEs.append(lse.cpu().numpy())
+    e_qf = torch.empty(T, device="cuda")
+    e_qf_layer = torch.empty((L, T), device="cuda")
+    topk = []
+    if k_per_video is not None:
+        kk = torch.tensor(list(k_per_video), dtype=torch.int32, device="cuda")
+        tk = torch.full((max(1, int(sum(k_per_video))),), -1,
+                        dtype=torch.int32, device="cuda")
+        ev.frame_evidence(mask, evid, L, e_qf, e_qf_layer=e_qf_layer,
+                          k_per_seq=kk, topk=tk)
+        torch.cuda.synchronize()
+        flat = tk.cpu().numpy()
+        off = 0
+        for k in k_per_video:
+            topk.append(flat[off:off + int(k)].astype(np.int64))
+            off += int(k)
+    else:
+        ev.frame_evidence(mask, evid, L, e_qf, e_qf_layer=e_qf_layer)
+        torch.cuda.synchronize()
+    return GpuRun(Os, LSEs, evid.cpu().numpy().astype(np.float64),
+                  tm.cpu().numpy().astype(np.float64),
+                  e_qf.cpu().numpy().astype(np.float64),
+                  e_qf_layer.cpu().numpy().astype(np.float64), topk, mask)
+
+
+def sample_rows(lay, n_visual, seed):
+    """All query-token rows plus a seeded sample of other rows."""
+    rng = np.random.default_rng(seed)
+    txt = lay.text_rows()
+    other = np.setdiff1d(np.arange(lay.S), txt)
+    pick = other if other.size <= n_visual else np.sort(
+        rng.choice(other, n_visual, replace=False))
+    return np.union1d(pick, txt)
+
+
+def output_error(O_gpu, O_ref, rows):
+    """max |O_gpu - O_ref| / max |O_ref| over ``rows``."""
+    g = O_gpu[rows].astype(np.float64)
+    return float(np.abs(g - O_ref).max() / max(np.abs(O_ref).max(), 1e-30))

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP probe (through the C ABI) against the fp64 oracle on
+the same seeded inputs.
+
+Tolerances: attention output max-abs error <= 2e-2 of the reference output's
+max magnitude; evidence and non-visual mass <= 1e-3 absolute per (layer,
+head, frame); LSE <= 2e-3 absolute (diagnostic); fp32 workloads are also held
+to 1e-4. Top-k frames must be identical wherever the oracle's score gap at
+rank k exceeds four times the propagated evidence tolerance, and the GPU's
+top-k must equal the oracle's ranking of the GPU's own pooled scores.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle.layout import Layout, Rule
+import workloads as wl
+from gpu_harness import run_gpu, sample_rows, output_error, say
+
+pytestmark = pytest.mark.gpu
+
+O_TOL, E_TOL, LSE_TOL = 2e-2, 1e-3, 2e-3
+
+
+def _lay_rule(w, seed=0):
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    return (Layout(ns, nf, nt, w.tokens_per_frame),
+            Rule(w.block, w.sink_blocks, w.window))
+
+
+def _check_layer(res, j, ref, rows, w, fp32_tight=False):
+    err = output_error(res.O[j], ref["O"], rows)
+    lse_err = float(np.abs(res.LSE[j][:, rows] - ref["LSE"]).max())
+    e_err = float(np.abs(res.E[j] - ref["E"]).max())
+    t_err = float(np.abs(res.text_mass[j] - ref["text_mass"]).max())
+    say(f"  layer {j}: O rel err {err:.2e}  LSE {lse_err:.2e}  "
+        f"E {e_err:.2e}  text_mass {t_err:.2e}")
+    assert err <= O_TOL
+    assert lse_err <= LSE_TOL
+    assert e_err <= E_TOL
+    assert t_err <= E_TOL
+    if fp32_tight:
+        assert err <= 1e-4 and e_err <= 1e-5 and lse_err <= 1e-5
+
+
+def _check_mass_invariant(res, lay):
+    for n in range(lay.n_seq):
+        f0, F = int(lay.frame0[n]), int(lay.n_frames[n])
+        tot = res.E[:, :, f0:f0 + F].sum(axis=2) + res.text_mass[:, :, n]
+        assert np.abs(tot - lay.n_text[n]).max() <= 1e-3 * max(
+            1, lay.n_text[n] / 64)
+
+
+def _check_topk(res, E_ref_all, lay, ks):
+    e_qf_ref, pooled = oracle.frame_evidence(E_ref_all, lay.n_frames,
+                                             lay.n_text)
+    tol_layer = E_TOL / np.repeat(lay.n_text, lay.n_frames)
+    assert np.all(np.abs(res.e_qf_layer - e_qf_ref) <= tol_layer + 1e-7)
+    assert np.all(np.abs(res.e_qf - pooled) <= tol_layer + 1e-7)
+    ref_top = oracle.topk_per_video(pooled, lay.n_frames, ks)
+    gaps = oracle.aggregate.boundary_gap(pooled, lay.n_frames, ks)
+    same_prec = oracle.topk_per_video(res.e_qf.astype(np.float32),
+                                      lay.n_frames, ks)
+    for n in range(lay.n_seq):
+        np.testing.assert_array_equal(res.topk[n], same_prec[n])
+        if gaps[n] > 4 * E_TOL / lay.n_text[n]:
+            np.testing.assert_array_equal(res.topk[n], ref_top[n])
+        else:
+            say(f"  video {n}: ambiguous top-{ks[n]} boundary "
+                f"(gap {gaps[n]:.2e}); identity not asserted")
+
+
+def _full_case(w, seed=0, ks=None):
+    lay, rule = _lay_rule(w, seed)
+    layers = list(range(w.n_layers))
+    ks = ks if ks is not None else [min(2, F) for F in lay.n_frames]
+    res = run_gpu(pytest.ev, w, layers, seed, k_per_video=ks)
+    E_all = []
+    for j, l in enumerate(layers):
+        q, k, v = wl.gen_layer(w, l, seed).as_f64()
+        ref = oracle.run_layer(q, k, v, lay, rule, w.softmax_scale)
+        _check_layer(res, j, ref, ref["rows"], w, fp32_tight=w.dtype == "fp32")
+        E_all.append(ref["E"])
+    _check_mass_invariant(res, lay)
+    _check_topk(res, np.stack(E_all), lay, ks)
+    return res
+
+
+@pytest.fixture(autouse=True)
+def _lib(gpu_lib):
+    pytest.ev = gpu_lib
+
+
+SMALL = {
+    # tiny fp32 workload of the probe (all-causal, 16-token frames)
+    "tiny_fp32": wl.get(1),
+    # ragged tails everywhere: system prefix, short last visual block,
+    # short query block; GQA 4:1; window 1
+    "ragged_sys_bf16": wl.get(2, name="ragged-sys", config_id=101, hq=4,
+                              hkv=1, n_frames=(7,), n_text=(37,), n_sys=(5,),
+                              tokens_per_frame=16, window=1,
+                              plant_args={"count": 2, "s_frame": (2.0, 2.0),
+                                          "s_query": 2.0}),
+    # three videos, split query rows (> 16 key blocks), d = 64
+    "multi_video_d64": wl.get(2, name="multi-d64", config_id=102, hq=6,
+                              hkv=2, d=64, n_frames=(40, 3, 45),
+                              n_text=(3, 70, 130), n_sys=(0, 9, 64),
+                              tokens_per_frame=32, window=2,
+                              plant_args={"count": 4, "s_frame": (2.0, 3.0),
+                                          "s_query": 2.0}),
+    # fp32 with d = 128, no sink, window 0, no GQA
+    "fp32_d128_w0": wl.get(1, name="fp32-d128", config_id=103, hq=2, hkv=2,
+                           d=128, n_frames=(20,), n_text=(65,),
+                           tokens_per_frame=16, sink_blocks=0, window=0,
+                           plant="choose",
+                           plant_args={"count": 2, "s_frame": (3.0, 3.0),
+                                       "s_query": 3.0}),
+    # 8-token frames (8 frames per key tile)
+    "nv8_bf16": wl.get(2, name="nv8", config_id=104, hq=7, hkv=1,
+                       n_frames=(50,), n_text=(20,), tokens_per_frame=8,
+                       window=3,
+                       plant_args={"count": 3, "s_frame": (3.0, 3.0),
+                                   "s_query": 3.0}),
+    # single frame, single query token
+    "degenerate": wl.get(2, name="degenerate", config_id=105, hq=2, hkv=1,
+                         n_frames=(1, 1), n_text=(1, 2), n_sys=(0, 3),
+                         tokens_per_frame=64,
+                         plant_args={"count": 1, "s_frame": (1.0, 1.0),
+                                     "s_query": 1.0}),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_parity_small(name):
+    say(f"case {name}")
+    _full_case(SMALL[name])
+
+
+def test_parity_single_layer_qwen_shape():
+    """128 frames x 64 tokens + 64 query tokens, 28/4 heads, d = 128."""
+    w = wl.get(2)
+    _, core, _ = wl.plant_table(w)
+    say("case config-2 single layer")
+    _full_case(w, ks=[len(core)])
+
+
+def _sampled_case(w, layers, seed=0, n_rows=2048):
+    import torch
+    lay, rule = _lay_rule(w, seed)
+    strength, core, _ = wl.plant_table(w, seed)
+    ks = []
+    for n in range(lay.n_seq):
+        f0, F = int(lay.frame0[n]), int(lay.n_frames[n])
+        ks.append(int(((core >= f0) & (core < f0 + F)).sum()))
+    refs = {}
+
+    def check(j, l, out, lse):
+        q, k, v = wl.gen_layer(w, l, seed).as_f64()
+        rows = sample_rows(lay, n_rows, seed=1000 + l)
+        ref = oracle.run_layer(q, k, v, lay, rule, w.softmax_scale, rows=rows)
+        rt = torch.from_numpy(rows).cuda()
+        o = out.index_select(0, rt).float().cpu().numpy()
+        ls = lse.index_select(1, rt).cpu().numpy()
+        err = float(np.abs(o - ref["O"]).max() / np.abs(ref["O"]).max())
+        lse_err = float(np.abs(ls - ref["LSE"]).max())
+        say(f"  layer {l}: O rel err {err:.2e}  LSE {lse_err:.2e}")
+        assert err <= O_TOL and lse_err <= LSE_TOL
+        refs[j] = ref
+
+    res = run_gpu(pytest.ev, w, layers, seed, k_per_video=ks, keep_o=False,
+                  on_layer=check)
+    E_all = np.stack([refs[j]["E"] for j in range(len(layers))])
+    TM_all = np.stack([refs[j]["text_mass"] for j in range(len(layers))])
+    e_err = float(np.abs(res.E - E_all).max())
+    t_err = float(np.abs(res.text_mass - TM_all).max())
+    say(f"  evidence err {e_err:.2e}  text_mass err {t_err:.2e}")
+    assert e_err <= E_TOL and t_err <= E_TOL
+    _check_mass_invariant(res, lay)
+    _check_topk(res, E_all, lay, ks)
+    return res
+
+
+def test_parity_28_layer_16k_probe():
+    """The 28-layer, 16,512-token probe the benchmark times: every layer,
+    all query rows plus 2048 sampled rows per layer, full evidence, top-16."""
+    say("case config-3 (28 layers)")
+    _sampled_case(wl.get(3), list(range(28)))
+
+
+def test_parity_long_video_two_layers():
+    """65,664 tokens (1024 frames), window 16: layers 0 and 27."""
+    say("case config-4 (layers 0, 27)")
+    w = wl.get(4)
+    _sampled_case(w, [0, 27], n_rows=1024)
+
+
+def test_parity_ragged_batch_two_layers():
+    """8 packed videos of 64-512 frames x 32 tokens: layers 0 and 13."""
+    say("case config-5 (layers 0, 13)")
+    _sampled_case(wl.get(5), [0, 13], n_rows=1024)
+
+
+def test_deterministic_bitwise():
+    w = wl.get(2)
+    say("case determinism")
+    a = run_gpu(pytest.ev, w, [0], k_per_video=[6])
+    b = run_gpu(pytest.ev, w, [0], k_per_video=[6])
+    assert np.array_equal(a.O[0], b.O[0])
+    assert np.array_equal(a.LSE[0], b.LSE[0])
+    assert np.array_equal(a.E, b.E)
+    assert np.array_equal(a.text_mass, b.text_mass)
+
+
+def test_onehot_values_reproduce_evidence():
+    """V = one-hot(frame) on visual keys, 0 elsewhere: the query rows'
+    outputs summed over rows equal the separately reduced evidence."""
+    w = wl.get(2)
+    lay, _ = _lay_rule(w)
+    assert w.d >= lay.T
+
+    def inputs(l):
+        base = wl.gen_layer(w, l)
+        v = np.zeros((lay.S, w.hkv, w.d), np.float32)
+        vis = np.nonzero(lay.frame >= 0)[0]
+        v[vis, :, lay.frame[vis]] = 1.0
+        return wl.Layer(base.q, base.k, wl.bf16_bits(v), base.u)
+
+    say("case one-hot V")
+    res = run_gpu(pytest.ev, w, [0], layer_inputs=inputs)
+    txt = lay.text_rows()
+    summed = res.O[0][txt].astype(np.float64).sum(axis=0)    # [Hq, d]
+    got = summed[:, :lay.T]
+    assert np.abs(got - res.E[0]).max() <= 1e-2 * max(1.0,
+                                                       np.abs(res.E[0]).max())

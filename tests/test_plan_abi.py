@@ -1,0 +1,148 @@
+"""Host-side checks of libevisel.so (no GPU): exported symbols, the plan's
+block partition and active pairs against the oracle's token predicate, the
+work list's coverage, and the documented error codes."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import blocks as oblocks
+from oracle.layout import Layout, Rule
+import workloads as wl
+import paper_2608_05780_amd as ev
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ev.LIB_PATH):
+        pytest.skip("libevisel.so not built (run __graft_entry__.build())")
+    return ev.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    hdr = open(os.path.join(ROOT, "include", "evisel.h")).read()
+    declared = set(re.findall(r"\b(evisel_[a-z_]+)\s*\(", hdr))
+    assert declared == set(ev.EXPORTED)
+    raw = ctypes.CDLL(ev.LIB_PATH)
+    for name in declared:
+        assert hasattr(raw, name), name
+
+
+def _plan(n_frames, n_text, Nv, rule, hq=4, hkv=2, n_sys=None):
+    return ev.build_block_mask(n_frames, n_text, Nv, rule.block,
+                               rule.sink_blocks, rule.window, hq, hkv,
+                               n_sys=n_sys, host_only=True)
+
+
+CASES = [
+    ((0,), (32,), (32,), 16, Rule(64, 1, -1)),
+    ((0,), (128,), (64,), 64, Rule(64, 1, 8)),
+    ((3, 0, 70), (9, 14, 5), (4, 64, 130), 32, Rule(64, 1, 2)),
+    ((5,), (23,), (9,), 16, Rule(32, 2, 3)),
+    ((0, 1), (7, 3), (3, 3), 4, Rule(8, 0, 1)),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(CASES)))
+def test_plan_matches_oracle_blocks(lib, ci):
+    ns, nf, nt, Nv, rule = CASES[ci]
+    m = _plan(nf, nt, Nv, rule, n_sys=ns)
+    lay = Layout(ns, nf, nt, Nv)
+    blk, rp, col = oblocks.active_csr(lay, rule, brute=lay.S < 3000)
+    got = ev.mask_export(m)
+    np.testing.assert_array_equal(got["start"], blk[:, 0])
+    np.testing.assert_array_equal(got["len"], blk[:, 1])
+    np.testing.assert_array_equal(got["region"], blk[:, 2])
+    np.testing.assert_array_equal(got["video"], blk[:, 3])
+    np.testing.assert_array_equal(got["row_ptr"], rp)
+    np.testing.assert_array_equal(got["col"], col)
+    st = m.stats
+    assert st["n_tokens"] == lay.S and st["n_frames_total"] == lay.T
+    assert st["n_text_rows"] == int(np.sum(nt))
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_workload_plans(lib, cid):
+    w = wl.get(cid)
+    ns, nf, nt = wl.layout_arrays(w)
+    rule = Rule(w.block, w.sink_blocks, w.window)
+    m = _plan(nf, nt, w.tokens_per_frame, rule, hq=w.hq, hkv=w.hkv, n_sys=ns)
+    got = ev.mask_export(m)
+    lay = Layout(ns, nf, nt, w.tokens_per_frame)
+    if cid <= 3:
+        blk, rp, col = oblocks.active_csr(lay, rule)
+        np.testing.assert_array_equal(got["row_ptr"], rp)
+        np.testing.assert_array_equal(got["col"], col)
+    expect = {1: 45, 2: 1364, 3: 3030, 4: 20330}
+    if cid in expect:
+        assert m.stats["n_active_pairs"] == expect[cid]
+    _check_work(m, got, w.hq)
+
+
+def _check_work(m, csr, hq):
+    wk = ev.mask_export_work(m)
+    region = csr["region"]
+    rp = csr["row_ptr"]
+    seen = {}
+    slots = set()
+    for qb, h, a, e, s in zip(wk["qblock"], wk["head"], wk["kb_begin"],
+                              wk["kb_end"], wk["slot"]):
+        if qb < 0:
+            continue
+        assert rp[qb] <= a < e <= rp[qb + 1]
+        seen.setdefault((int(qb), int(h)), []).append((int(a), int(e)))
+        if region[qb] == 2:
+            assert s >= 0 and s not in slots
+            slots.add(int(s))
+        else:
+            assert s == -1 and (a, e) == (rp[qb], rp[qb + 1])
+    nb = len(region)
+    assert len(seen) == nb * hq
+    for (qb, h), runs in seen.items():
+        runs.sort()
+        assert runs[0][0] == rp[qb] and runs[-1][1] == rp[qb + 1]
+        for (a0, e0), (a1, e1) in zip(runs, runs[1:]):
+            assert e0 == a1
+    assert len(slots) == m.stats["n_chunk_slots"]
+    assert slots == set(range(m.stats["n_chunk_slots"]))
+
+
+def _status(fn):
+    with pytest.raises(ev.EviselError) as ei:
+        fn()
+    return ei.value.status
+
+
+def test_error_codes(lib):
+    r = Rule(64, 1, 8)
+    assert _status(lambda: _plan([4], [2], 64, r, hq=6, hkv=4)) == \
+        ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([0], [2], 64, r)) == ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [0], 64, r)) == ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 0, r)) == ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, Rule(0, 1, 8))) == \
+        ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, Rule(64, -1, 8))) == \
+        ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, Rule(64, 1, -2))) == \
+        ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, r, n_sys=[-1])) == \
+        ev.ERR_INVALID_ARG
+    # compute calls refuse a host-only plan before touching the device
+    m = _plan([3], [2], 64, r)
+    st = lib.evisel_sparse_prefill(m.handle, 0, 1, None, None, None, 128, 0,
+                                   0.1, None, None, None, None, None, 0, None)
+    assert st == ev.ERR_INVALID_ARG
+    assert b"device" in lib.evisel_last_error()
+    st = lib.evisel_frame_evidence(m.handle, None, 1, None, None, None, None,
+                                   None)
+    assert st == ev.ERR_INVALID_ARG
+    assert lib.evisel_sparse_prefill_workspace(m.handle, 96) == 0
+    assert lib.evisel_sparse_prefill_workspace(m.handle, 128) > 0
+    assert lib.evisel_mask_info(None, None) == ev.ERR_INVALID_ARG
+    lib.evisel_mask_free(None)                   # ignored

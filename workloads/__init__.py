@@ -13,8 +13,12 @@ paper's appendix on sparse prefilling.
 Draw protocol (fixed, so the oracle and the GPU see bit-identical inputs):
 
 * ``SeedSequence([seed, config_id]).spawn(n_layers + 1)``: child 0 draws the
-  plant table (and, for the ragged batch, the frame counts); child l+1 draws
-  layer l in the order Q, K, V, u with ``Generator(PCG64)``.
+  plant table (and, for the ragged batch, the frame counts); child l+1 is
+  spawned again into 3 * CHUNKS + 1 streams for layer l: the token range is
+  cut into CHUNKS equal parts, and part c of Q, K and V is filled from
+  streams c, CHUNKS + c and 2 * CHUNKS + c; the last stream draws u. Each
+  stream is a ``Generator(PCG64)``; the parts are filled by a thread pool,
+  which does not change any value.
 * Q ``[S, Hq, d]``, K and V ``[S, Hkv, d]`` are i.i.d. N(0, 1) float32; u is a
   unit vector in R^d (float32).
 * Planting: every kv head's K rows of a planted frame f get ``+ s_f * u`` and
@@ -27,7 +31,12 @@ from __future__ import annotations
 from dataclasses import dataclass, field
 from typing import Optional
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
+
+CHUNKS = 8
 
 __all__ = ["Workload", "CONFIGS", "get", "layout_arrays", "plant_table",
            "gen_layer", "bf16_bits", "bf16_bits_to_f32", "Layer"]
@@ -95,9 +104,9 @@ CONFIGS = {
 }
 
 
-def get(config_id: int, **overrides) -> Workload:
-    """Return a configured workload, optionally with fields replaced."""
-    w = CONFIGS[config_id]
+def get(cid: int, **overrides) -> Workload:
+    """Return workload ``cid``, optionally with fields replaced."""
+    w = CONFIGS[cid]
     if overrides:
         kw = dict(w.__dict__)
         kw.update(overrides)
@@ -199,7 +208,20 @@ def plant_table(w: Workload, seed: int = 0):
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
-    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    """float32 -> bf16 bit patterns (uint16), round to nearest even.
+
+    Uses torch's (multithreaded, round-to-nearest-even) conversion when
+    available; ``bf16_bits_numpy`` is the same rounding written out."""
+    try:
+        import torch
+    except ImportError:
+        return bf16_bits_numpy(x)
+    t = torch.from_numpy(np.ascontiguousarray(x, np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def bf16_bits_numpy(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns by integer round-to-nearest-even."""
     u = np.ascontiguousarray(x, np.float32).view(np.uint32)
     r = ((u + np.uint32(0x7FFF) + ((u >> 16) & np.uint32(1))) >> 16)
     return r.astype(np.uint16)
@@ -248,10 +270,24 @@ def gen_layer(w: Workload, layer: int, seed: int = 0,
     ns, nf, nt = layout_arrays(w, seed)
     tok0, vis0, txt0, end = token_ranges(w, seed)
     S = int(end[-1])
-    rng = np.random.Generator(np.random.PCG64(_streams(w, seed)[layer + 1]))
-    q = rng.standard_normal((S, w.hq, w.d), dtype=np.float32)
-    k = rng.standard_normal((S, w.hkv, w.d), dtype=np.float32)
-    v = rng.standard_normal((S, w.hkv, w.d), dtype=np.float32)
+    kids = _streams(w, seed)[layer + 1].spawn(3 * CHUNKS + 1)
+    q = np.empty((S, w.hq, w.d), np.float32)
+    k = np.empty((S, w.hkv, w.d), np.float32)
+    v = np.empty((S, w.hkv, w.d), np.float32)
+    cuts = [S * c // CHUNKS for c in range(CHUNKS + 1)]
+
+    def fill(job):
+        arr, c, kid = job
+        a, b = cuts[c], cuts[c + 1]
+        if b > a:
+            np.random.Generator(np.random.PCG64(kid)).standard_normal(
+                dtype=np.float32, out=arr[a:b])
+
+    jobs = [(arr, c, kids[t * CHUNKS + c])
+            for t, arr in enumerate((q, k, v)) for c in range(CHUNKS)]
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(fill, jobs))
+    rng = np.random.Generator(np.random.PCG64(kids[3 * CHUNKS]))
     u = rng.standard_normal(w.d, dtype=np.float32).astype(np.float64)
     u = (u / np.linalg.norm(u)).astype(np.float32)
     strength, _, s_q = plant_table(w, seed)
