@@ -71,6 +71,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes "
+                         "(3 times), to scale HBM byte counters")
     args = ap.parse_args()
     world, rank = _world()
     if args.gpus != 1 or world != 1:
@@ -87,8 +90,17 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
-    ev.load()
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy // 4
+        x = torch.ones(n, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 3}))
+        return
+    ev.load()
     w = wl.get(args.config)
     L = w.n_layers
     ns, nf, nt = wl.layout_arrays(w, args.seed)

@@ -94,13 +94,18 @@ def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
                   e_qf_layer.cpu().numpy().astype(np.float64), topk, mask)
 
 
-def sample_rows(lay, n_visual, seed):
-    """All query-token rows plus a seeded sample of other rows."""
+def sample_rows(lay, n_rows, seed, run=64):
+    """All query-token rows plus about ``n_rows`` other rows, drawn as
+    seeded runs of ``run`` consecutive tokens at random offsets (so they
+    straddle block boundaries)."""
     rng = np.random.default_rng(seed)
     txt = lay.text_rows()
     other = np.setdiff1d(np.arange(lay.S), txt)
-    pick = other if other.size <= n_visual else np.sort(
-        rng.choice(other, n_visual, replace=False))
+    if other.size <= n_rows:
+        return np.union1d(other, txt)
+    starts = rng.choice(other.size - run, size=max(1, n_rows // run),
+                        replace=False)
+    pick = np.unique(np.concatenate([other[s:s + run] for s in starts]))
     return np.union1d(pick, txt)
 
 
