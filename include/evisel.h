@@ -120,12 +120,14 @@ evisel_status evisel_mask_export(const evisel_mask* mask, int32_t* blk_start,
                                  int32_t* col);
 
 /* Copies the attention work list (n_work_items entries) in launch order:
- * query block, query head, first and one-past-last CSR position of its key
- * blocks, and split slot (-1 unless it is part of a split query-token row).
- * Any pointer may be NULL. */
+ * query block (-1 for padding), first query head, number of query heads
+ * (consecutive, sharing one kv head), first and one-past-last CSR position
+ * of its key blocks, and the first head's split slot (-1 unless the item is
+ * part of a split query-token row). Any pointer may be NULL. */
 evisel_status evisel_mask_export_work(const evisel_mask* mask, int32_t* qblock,
-                                      int32_t* head, int32_t* kb_begin,
-                                      int32_t* kb_end, int32_t* slot);
+                                      int32_t* head, int32_t* nheads,
+                                      int32_t* kb_begin, int32_t* kb_end,
+                                      int32_t* slot);
 
 /* Bytes of device workspace evisel_sparse_prefill needs for head dim d. */
 size_t evisel_sparse_prefill_workspace(const evisel_mask* mask, int32_t d);

@@ -65,7 +65,7 @@ _SIGS = {
     "evisel_mask_info": (ctypes.c_int, [ctypes.c_void_p,
                                         ctypes.POINTER(_Stats)]),
     "evisel_mask_export": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 6),
-    "evisel_mask_export_work": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 5),
+    "evisel_mask_export_work": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 6),
     "evisel_sparse_prefill_workspace": (ctypes.c_size_t, [ctypes.c_void_p,
                                                           ctypes.c_int32]),
     "evisel_sparse_prefill": (ctypes.c_int, [
@@ -201,13 +201,12 @@ def mask_export(mask: Mask) -> dict:
 def mask_export_work(mask: Mask) -> dict:
     import numpy as np
     n = mask.stats["n_work_items"]
-    out = {k: np.zeros(max(n, 1), np.int32) for k in ("qblock", "head",
-                                                      "kb_begin", "kb_end",
-                                                      "slot")}
+    out = {k: np.zeros(max(n, 1), np.int32) for k in (
+        "qblock", "head", "nheads", "kb_begin", "kb_end", "slot")}
     p = lambda a: a.ctypes.data_as(_i32p)
-    _check(load().evisel_mask_export_work(mask.handle, p(out["qblock"]),
-                                          p(out["head"]), p(out["kb_begin"]),
-                                          p(out["kb_end"]), p(out["slot"])))
+    _check(load().evisel_mask_export_work(
+        mask.handle, p(out["qblock"]), p(out["head"]), p(out["nheads"]),
+        p(out["kb_begin"]), p(out["kb_end"]), p(out["slot"])))
     return {k: v[:n] for k, v in out.items()}
 
 

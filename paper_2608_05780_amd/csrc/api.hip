@@ -245,13 +245,15 @@ evisel_status evisel_mask_export(const evisel_mask* m, int32_t* blk_start,
 }
 
 evisel_status evisel_mask_export_work(const evisel_mask* m, int32_t* qblock,
-                                      int32_t* head, int32_t* kb_begin,
-                                      int32_t* kb_end, int32_t* slot) {
+                                      int32_t* head, int32_t* nheads,
+                                      int32_t* kb_begin, int32_t* kb_end,
+                                      int32_t* slot) {
   if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
   const auto& it = m->plan.items;
   for (size_t i = 0; i < it.size(); ++i) {
     if (qblock) qblock[i] = it[i].qblock;
     if (head) head[i] = it[i].head;
+    if (nheads) nheads[i] = it[i].nheads;
     if (kb_begin) kb_begin[i] = it[i].kb_begin;
     if (kb_end) kb_end[i] = it[i].kb_end;
     if (slot) slot[i] = it[i].slot;

@@ -1,15 +1,25 @@
 // Block-sparse prefill attention for gfx950 with fused query-frame evidence
 // partials, and the combine step of split query-token rows.
 //
-// Work item = one query block (a region block of <= 64 tokens), one query
-// head and a run of that block's active key blocks (CSR). A work-group of two
-// wavefronts owns the item; each wavefront owns 32 query rows.
+// Work item = one query block (a region block of <= 64 tokens), up to two
+// query heads sharing one kv head, and a run of the block's active key
+// blocks (CSR). A work-group has four wavefronts: waves 0-1 take the first
+// head's rows 0-31 / 32-63, waves 2-3 the second head's. Each key/value tile
+// is staged once in LDS for both heads. Two work-groups fit a CU, so every
+// SIMD interleaves two wavefronts: one's softmax VALU work overlaps the
+// other's MFMA work.
+//
+// Key/value tiles go straight from global memory to LDS (16-byte
+// global_load_lds per lane, no staging registers), double-buffered: tile j+1
+// is in flight while tile j is computed, one barrier per tile. Rows are
+// XOR-swizzled in 16-byte chunks so the MFMA operand reads below are free of
+// LDS bank conflicts.
 //
 // Per key tile (64 keys):
 //   S^T = K Q^T        32x32x16 bf16 MFMA (fp32 inputs: 32x32x2 f32 MFMA);
 //                      computing the transpose leaves one query row per lane
-//                      (lane % 32), so row reductions stay inside the lane
-//                      plus one exchange with lane ^ 32.
+//                      (lane % 32); a row max or sum is an in-lane reduction
+//                      plus one v_permlane32_swap with lane ^ 32.
 //   mask               only on tiles reaching past the first query row or
 //                      shorter than 64 keys: keys after the row (causal) and
 //                      past the block end.
@@ -24,9 +34,10 @@
 //                      (system prefix, query tokens) accumulate into one
 //                      running partial per item.
 //   O^T += V^T P^T     P rounded to bf16 (RNE) as the B operand straight from
-//                      the S^T registers; V^T staged transposed in LDS.
-// Key/value tiles are prefetched into registers during the previous tile's
-// math and written to LDS between two barriers.
+//                      the S^T registers; the V^T operand comes from the
+//                      row-major V tile through ds_read_b64_tr_b16 (LDS
+//                      transpose read: within 16 lanes, lane i receives
+//                      element i % 4 of the rows addressed by lanes i/4 + 4k).
 //
 // Visual and system rows finish in the kernel (O, LSE). Query-token rows are
 // split into chunks of key blocks (longest-first balance across the chip);
@@ -34,17 +45,20 @@
 // mass) in the workspace and the combine kernel merges them.
 #include "kernels.h"
 
+#define EV_LDS __attribute__((address_space(3)))
+
 namespace evisel {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 64;
-constexpr int kWaves = 2;
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
@@ -56,24 +70,58 @@ __device__ __forceinline__ float exp2_(float x) {
 __device__ __forceinline__ float log2_(float x) {
   return __builtin_amdgcn_logf(x);
 }
-__device__ __forceinline__ float partner(float x) { return __shfl_xor(x, 32); }
+// v_permlane32_swap(x, x) returns (x[lane], x[lane ^ 32]) in some order on
+// every lane, so the pair's sum and max need no LDS round trip.
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                            __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                            __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// 16-byte chunk swizzles of a 64-row LDS tile: physical chunk = logical
+// chunk ^ swz(row).
+enum Swz { kSwzK = 0, kSwzV = 1, kSwzNone = 2 };
+template <int SWZ>
+__device__ __forceinline__ int swz(int row) {
+  return SWZ == kSwzK ? (row & 7) : SWZ == kSwzV ? ((row & 3) << 1) : 0;
+}
+
+// Issues the loads of one 64-key tile of a [S][H][D] tensor (head kvh) into
+// LDS: every thread fetches 64*RC/256 chunks of 16 bytes; a wavefront's load
+// fills 64 consecutive 16-byte LDS slots. Rows past klen re-read the last
+// valid row (finite values; they are masked to zero probability).
+template <typename T, int D, int SWZ>
+__device__ __forceinline__ void issue_tile(EV_LDS char* buf, const T* src,
+                                           int kstart, int klen, int kvh,
+                                           int hkv, int wave, int lane) {
+  constexpr int RC = D * (int)sizeof(T) / 16;
+  constexpr int N = kTile * RC / kThreads;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const int slot = (wave * N + i) * 64 + lane;
+    const int row = slot / RC;
+    const int ch = (slot % RC) ^ swz<SWZ>(row);
+    const int srow = row < klen ? row : klen - 1;
+    const char* g =
+        (const char*)(src + ((size_t)(kstart + srow) * hkv + kvh) * D) +
+        ch * 16;
+    __builtin_amdgcn_global_load_lds((const void*)g,
+                                     (EV_LDS void*)(buf + (wave * N + i) * 1024),
+                                     16, 0, 0);
+  }
+}
 
 // ---------------------------------------------------------------------------
-// bf16 operands: Q fragment in registers, K [key][d] and V^T [d][key] in LDS.
+// bf16 operands.
 template <int D>
 struct Bf16Path {
-  static constexpr int KS = D + 8;       // padded K row (elements)
-  static constexpr int VS = kTile + 4;   // padded V^T row (elements)
-  static constexpr int KCH = kTile * D / 8 / kThreads;  // 16-B K chunks
-  static constexpr int VGR = 16 * (D / 8) / kThreads;   // 4x8 V groups
-  struct Smem {
-    __bf16 k[kTile * KS];
-    __bf16 vt[D * VS];
-  };
-  struct Stage {
-    bf16x8 k[KCH];
-    bf16x8 v[VGR][4];
-  };
+  using T = __bf16;
+  static constexpr int RC = D / 8;   // 16-byte chunks per row
   struct QFrag {
     bf16x8 x[D / 16];
   };
@@ -88,67 +136,17 @@ struct Bf16Path {
     }
   }
 
-  __device__ static void fetch(Stage& st, const void* k, const void* v,
-                               int kstart, int klen, int kvh, int hkv,
-                               int tid) {
-    const __bf16* kb = (const __bf16*)k;
-    const __bf16* vb = (const __bf16*)v;
-#pragma unroll
-    for (int r = 0; r < KCH; ++r) {
-      const int c = tid + kThreads * r;
-      const int row = c / (D / 8), c8 = c % (D / 8);
-      bf16x8 z = {};
-      st.k[r] = row < klen
-                    ? *(const bf16x8*)(kb + ((size_t)(kstart + row) * hkv +
-                                             kvh) * D + c8 * 8)
-                    : z;
-    }
-#pragma unroll
-    for (int r = 0; r < VGR; ++r) {
-      const int gi = tid + kThreads * r;
-      const int kq = gi % 16, cc = gi / 16;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 4 * kq + i;
-        bf16x8 z = {};
-        st.v[r][i] = row < klen
-                         ? *(const bf16x8*)(vb + ((size_t)(kstart + row) * hkv +
-                                                  kvh) * D + cc * 8)
-                         : z;
-      }
-    }
-  }
-
-  __device__ static void commit(Smem& sm, const Stage& st, const void*,
-                                const void*, int, int, int, int, int tid) {
-#pragma unroll
-    for (int r = 0; r < KCH; ++r) {
-      const int c = tid + kThreads * r;
-      const int row = c / (D / 8), c8 = c % (D / 8);
-      *(bf16x8*)&sm.k[row * KS + c8 * 8] = st.k[r];
-    }
-#pragma unroll
-    for (int r = 0; r < VGR; ++r) {
-      const int gi = tid + kThreads * r;
-      const int kq = gi % 16, cc = gi / 16;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x4 t = {st.v[r][0][e], st.v[r][1][e], st.v[r][2][e],
-                    st.v[r][3][e]};
-        *(bf16x4*)&sm.vt[(8 * cc + e) * VS + 4 * kq] = t;
-      }
-    }
-  }
-
-  // S^T[key][q] for the two 32-key halves of the tile.
-  __device__ static void qk(f32x16 (&s)[2], const Smem& sm, const QFrag& qf,
-                            int l32, int g) {
+  // S^T[key][q] for the two 32-key halves of the tile: lane (key, g) reads
+  // logical chunk 2kk + g of K row key.
+  __device__ static void qk(f32x16 (&s)[2], const EV_LDS char* kt,
+                            const QFrag& qf, int l32, int g) {
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const bf16x8 kf =
-            *(const bf16x8*)&sm.k[(32 * c + l32) * KS + 16 * kk + 8 * g];
+        const int key = 32 * c + l32;
+        const int ch = (2 * kk + g) ^ swz<kSwzK>(key);
+        const bf16x8 kf = *(const EV_LDS bf16x8*)(kt + (key * RC + ch) * 16);
         s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf.x[kk], s[c], 0,
                                                         0, 0);
       }
@@ -157,9 +155,15 @@ struct Bf16Path {
 
   // O^T[d][q] += V^T[d][key] P^T[key][q]. The B operand of k-step (c, s)
   // is the lane's own s[c][8s .. 8s+7], i.e. keys 32c + 16s + 8(e/4) +
-  // 4g + e%4 for e = 0..7; the A operand reads V^T at the same keys.
-  __device__ static void pv(f32x16 (&o)[D / 32], const Smem& sm,
-                            const f32x16 (&p)[2], int l32, int g) {
+  // 4g + e%4 for e = 0..7. The A operand for d-tile mt: two transpose reads
+  // in which lane j of each 16-lane group addresses V row
+  // 32c + 16s + 4g + j/4 (+8 for the second) at column
+  // 32mt + 16((lane/16) % 2) + 4(j % 4); lane i then holds V[those 4 keys]
+  // at column 32mt + lane % 32.
+  __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
+                            const f32x16 (&p)[2], int lane) {
+    const int j = lane & 15, q16 = lane >> 4, g = lane >> 5;
+    const int sw = (j >> 2) << 1;   // swz<kSwzV>(row): row % 4 == j / 4
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
 #pragma unroll
@@ -169,13 +173,19 @@ struct Bf16Path {
                                 : __builtin_shufflevector(p[c], p[c], 8, 9, 10,
                                                           11, 12, 13, 14, 15);
         const bf16x8 pb = __builtin_convertvector(pf, bf16x8);
+        const int row = 32 * c + 16 * s + 4 * g + (j >> 2);
 #pragma unroll
         for (int mt = 0; mt < D / 32; ++mt) {
-          const __bf16* row = &sm.vt[(32 * mt + l32) * VS + 32 * c + 16 * s];
-          const bf16x4 lo = *(const bf16x4*)(row + 4 * g);
-          const bf16x4 hi = *(const bf16x4*)(row + 8 + 4 * g);
-          const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5,
-                                                    6, 7);
+          const int col = 32 * mt + 16 * (q16 & 1) + 4 * (j & 3);
+          const int ch = (col >> 3) ^ sw;
+          const EV_LDS char* a0 = vt + (row * RC + ch) * 16 + 8 * (j & 1);
+          const EV_LDS char* a1 = a0 + 8 * RC * 16;   // row + 8
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (EV_LDS i16x4*)a0);
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (EV_LDS i16x4*)a1);
+          const i16x4 lohi[2] = {lo, hi};
+          const bf16x8 va = __builtin_bit_cast(bf16x8, lohi);
           o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[mt], 0, 0,
                                                           0);
         }
@@ -196,13 +206,8 @@ struct Bf16Path {
 // V needs no transpose: each lane contributes one value per k-step.
 template <int D>
 struct F32Path {
-  static constexpr int KS = D + 4;
-  static constexpr int VS = D + 4;
-  struct Smem {
-    float k[kTile * KS];
-    float v[kTile * VS];
-  };
-  struct Stage {};
+  using T = float;
+  static constexpr int RC = D / 4;
   struct QFrag {
     float x[D / 2];
   };
@@ -215,47 +220,30 @@ struct F32Path {
       f32x4 z = {};
       const f32x4 t = ok ? *(const f32x4*)(src + 4 * u) : z;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) qf.x[4 * u + j] = t[j];
+      for (int jj = 0; jj < 4; ++jj) qf.x[4 * u + jj] = t[jj];
     }
   }
 
-  __device__ static void fetch(Stage&, const void*, const void*, int, int, int,
-                               int, int) {}
-
-  __device__ static void commit(Smem& sm, const Stage&, const void* k,
-                                const void* v, int kstart, int klen, int kvh,
-                                int hkv, int tid) {
-    const float* kb = (const float*)k;
-    const float* vb = (const float*)v;
-    for (int c = tid; c < kTile * D / 4; c += kThreads) {
-      const int row = c / (D / 4), c4 = c % (D / 4);
-      f32x4 z = {};
-      const size_t off = ((size_t)(kstart + row) * hkv + kvh) * D + c4 * 4;
-      *(f32x4*)&sm.k[row * KS + c4 * 4] =
-          row < klen ? *(const f32x4*)(kb + off) : z;
-      *(f32x4*)&sm.v[row * VS + c4 * 4] =
-          row < klen ? *(const f32x4*)(vb + off) : z;
-    }
-  }
-
-  __device__ static void qk(f32x16 (&s)[2], const Smem& sm, const QFrag& qf,
-                            int l32, int g) {
+  __device__ static void qk(f32x16 (&s)[2], const EV_LDS char* kt,
+                            const QFrag& qf, int l32, int g) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
+      const int key = 32 * c + l32;
 #pragma unroll
       for (int u = 0; u < D / 8; ++u) {
-        const f32x4 kf =
-            *(const f32x4*)&sm.k[(32 * c + l32) * KS + g * D / 2 + 4 * u];
+        const int ch = (g * D / 8 + u) ^ swz<kSwzK>(key);
+        const f32x4 kf = *(const EV_LDS f32x4*)(kt + (key * RC + ch) * 16);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          s[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf[j], qf.x[4 * u + j],
+        for (int jj = 0; jj < 4; ++jj)
+          s[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf[jj], qf.x[4 * u + jj],
                                                       s[c], 0, 0, 0);
       }
     }
   }
 
-  __device__ static void pv(f32x16 (&o)[D / 32], const Smem& sm,
-                            const f32x16 (&p)[2], int l32, int g) {
+  __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
+                            const f32x16 (&p)[2], int lane) {
+    const int l32 = lane & 31, g = lane >> 5;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
 #pragma unroll
@@ -264,7 +252,8 @@ struct F32Path {
 #pragma unroll
         for (int mt = 0; mt < D / 32; ++mt)
           o[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-              sm.v[key * VS + 32 * mt + l32], p[c][r], o[mt], 0, 0, 0);
+              *(const EV_LDS float*)(vt + key * RC * 16 + (32 * mt + l32) * 4),
+              p[c][r], o[mt], 0, 0, 0);
       }
     }
   }
@@ -277,22 +266,32 @@ struct F32Path {
 
 // ---------------------------------------------------------------------------
 template <class P, int D>
-__global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
-                                                        const Workspace ws,
-                                                        const AttnCall ac) {
-  __shared__ typename P::Smem sm;
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+                          amdgpu_waves_per_eu(2, 2))) void
+attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
+  using T = typename P::T;
+  constexpr int TB = kTile * P::RC * 16;   // bytes of one tile
+  constexpr int VSWZ = sizeof(T) == 2 ? kSwzV : kSwzNone;
+  __shared__ __attribute__((aligned(1024))) char smem[4 * TB];
+  EV_LDS char* lds = (EV_LDS char*)smem;   // [K0 | V0 | K1 | V1]
+
   const WorkItem it = pl.items[blockIdx.x];
   if (it.qblock < 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, g = lane >> 5;
+  const int hsub = wave >> 1;
+  const bool active = hsub < it.nheads;
+  const int h = it.head + (active ? hsub : 0);
+  const int kvh = it.head / (pl.hq / pl.hkv);
   const BlockDesc qb = pl.blocks[it.qblock];
-  const int h = it.head, kvh = h / (pl.hq / pl.hkv);
   const bool is_text = it.slot >= 0;
-  const int qrow = 32 * wave + l32;
-  const bool qvalid = qrow < qb.len;
+  const int qrow = 32 * (wave & 1) + l32;
+  const bool qvalid = active && qrow < qb.len;
   const int qpos = qb.start + qrow;
   const int n = it.kb_end - it.kb_begin;
   const float c2 = ac.scale_log2;
+  const T* kg = (const T*)ac.k;
+  const T* vg = (const T*)ac.v;
 
   typename P::QFrag qf;
   P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
@@ -302,22 +301,29 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) o[i] = f32x16{};
 
-  typename P::Stage st;
   BlockDesc kb = pl.blocks[pl.col[it.kb_begin]];
-  P::fetch(st, ac.k, ac.v, kb.start, kb.len, kvh, pl.hkv, tid);
+  issue_tile<T, D, kSwzK>(lds, kg, kb.start, kb.len, kvh, pl.hkv, wave, lane);
+  issue_tile<T, D, VSWZ>(lds + TB, vg, kb.start, kb.len, kvh, pl.hkv, wave,
+                         lane);
 
   for (int j = 0; j < n; ++j) {
-    __syncthreads();
-    P::commit(sm, st, ac.k, ac.v, kb.start, kb.len, kvh, pl.hkv, tid);
-    __syncthreads();
     const BlockDesc cur = kb;
+    const EV_LDS char* kt = lds + (j & 1) * 2 * TB;
+    const EV_LDS char* vt = kt + TB;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
     if (j + 1 < n) {
       kb = pl.blocks[pl.col[it.kb_begin + j + 1]];
-      P::fetch(st, ac.k, ac.v, kb.start, kb.len, kvh, pl.hkv, tid);
+      EV_LDS char* nk = lds + ((j + 1) & 1) * 2 * TB;
+      issue_tile<T, D, kSwzK>(nk, kg, kb.start, kb.len, kvh, pl.hkv, wave,
+                              lane);
+      issue_tile<T, D, VSWZ>(nk + TB, vg, kb.start, kb.len, kvh, pl.hkv,
+                             wave, lane);
     }
+    if (!active) continue;
 
     f32x16 s[2] = {f32x16{}, f32x16{}};
-    P::qk(s, sm, qf, l32, g);
+    P::qk(s, kt, qf, l32, g);
 
     if (cur.len < kTile || cur.start + cur.len - 1 > qb.start) {
 #pragma unroll
@@ -334,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[c][r]);
-    mx = fmaxf(mx, partner(mx));
+    mx = pair_max(mx);
     const float m_new = fmaxf(m_ref, mx * c2);
     const bool need = m_new > m_ref + kRescaleSlack;
     if (__any(need)) {
@@ -368,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
 #pragma unroll
           for (int r = 0; r < 16; ++r) g8[4 * c + (r >> 2)] += s[c][r];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) g8[q] += partner(g8[q]);
+        for (int q = 0; q < 8; ++q) g8[q] = pair_sum(g8[q]);
         const int lg = __builtin_ctz((unsigned)pl.Nv) - 3;  // log2(N_v / 8)
         const int nseg = kTile / pl.Nv;
         const SeqDesc sq = pl.seqs[it.seq];
@@ -387,10 +393,11 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
       }
     }
 
-    P::pv(o, sm, s, l32, g);
+    P::pv(o, vt, s, lane);
   }
+  if (!active) return;
 
-  const float l_tot = l_part + partner(l_part);
+  const float l_tot = pair_sum(l_part);
   if (!is_text) {
     if (qvalid) {
       const float inv = 1.f / l_tot;
@@ -406,9 +413,10 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
         ac.lse[(size_t)h * pl.S + qpos] = (m_ref + log2_(l_tot)) * kLn2;
     }
   } else {
-    const float nv_tot = nv_part + partner(nv_part);
+    const float nv_tot = pair_sum(nv_part);
+    const int slot = it.slot + hsub * it.nch;
     if (qvalid) {
-      float* po = ws.pO + ((size_t)it.slot * kTile + qrow) * D;
+      float* po = ws.pO + ((size_t)slot * kTile + qrow) * D;
 #pragma unroll
       for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
@@ -418,7 +426,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(const DevPlan pl,
           *(f32x4*)(po + 32 * mt + 8 * r4 + 4 * g) = v;
         }
       if (g == 0) {
-        const size_t ix = (size_t)it.slot * kTile + qrow;
+        const size_t ix = (size_t)slot * kTile + qrow;
         ws.pM[ix] = m_ref;
         ws.pL[ix] = l_tot;
         ws.pNV[ix] = nv_tot > 0.f ? m_ref + log2_(nv_tot) : neg_inf();

@@ -132,9 +132,11 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     return "internal error: CSR size mismatch";
 
   // ---- work items ---------------------------------------------------------
+  const int32_t group = hq / hkv;
+  const int32_t pairs = (group + kHeadsPerItem - 1) / kHeadsPerItem;
   int64_t total = 0;
   for (int32_t b = 0; b < nb; ++b)
-    total += (int64_t)(P.row_ptr[b + 1] - P.row_ptr[b]) * hq;
+    total += (int64_t)(P.row_ptr[b + 1] - P.row_ptr[b] + 1) * hkv * pairs;
   const int64_t avg = (total + kTargetSlots - 1) / kTargetSlots;
   P.chunk_blocks = (int32_t)std::max<int64_t>(16, avg);
 
@@ -148,27 +150,33 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
       if (P.seqs[n].n_tiles == 0) P.seqs[n].tile0 = (int32_t)P.tiles.size();
       P.seqs[n].n_tiles++;
       P.tiles.push_back(tt);
-      for (int32_t h = 0; h < hq; ++h)
-        for (int32_t c = 0; c < nch; ++c) {
-          // equal-size chunks: chunk c covers [rb + c*len/nch, ...)
-          const int32_t a = rb + (int32_t)((int64_t)c * len / nch);
-          const int32_t e = rb + (int32_t)((int64_t)(c + 1) * len / nch);
-          WorkItem w{b, h, a, e, tt.slot0 + h * nch + c, (int32_t)n, c, 0};
-          txt_items.push_back({w, e - a});
+      for (int32_t g = 0; g < hkv; ++g)
+        for (int32_t pp = 0; pp < pairs; ++pp) {
+          const int32_t h0 = g * group + pp * kHeadsPerItem;
+          const int32_t nh = std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
+          for (int32_t c = 0; c < nch; ++c) {
+            // equal-size chunks: chunk c covers [rb + c*len/nch, ...)
+            const int32_t a = rb + (int32_t)((int64_t)c * len / nch);
+            const int32_t e = rb + (int32_t)((int64_t)(c + 1) * len / nch);
+            WorkItem w{b, h0, nh, a, e, tt.slot0 + h0 * nch + c, (int32_t)n,
+                       nch};
+            txt_items.push_back({w, e - a + 1});
+          }
         }
       P.n_slots += (int64_t)hq * nch;
     }
-    // visual and system rows, ordered by (kv head, block, head) so that
+    // visual and system rows, ordered by (kv head, block, head pair) so that
     // neighbouring launches share key/value tiles
-    const int32_t group = hq / hkv;
     for (int32_t g = 0; g < hkv; ++g) {
       auto add = [&](const std::vector<int32_t>& ids) {
         for (int32_t b : ids)
-          for (int32_t hh = 0; hh < group; ++hh) {
-            const int32_t h = g * group + hh;
-            WorkItem w{b, h, P.row_ptr[b], P.row_ptr[b + 1], -1, (int32_t)n,
-                       0, 0};
-            other_items.push_back({w, P.row_ptr[b + 1] - P.row_ptr[b]});
+          for (int32_t pp = 0; pp < pairs; ++pp) {
+            const int32_t h0 = g * group + pp * kHeadsPerItem;
+            const int32_t nh =
+                std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
+            WorkItem w{b, h0, nh, P.row_ptr[b], P.row_ptr[b + 1], -1,
+                       (int32_t)n, 0};
+            other_items.push_back({w, P.row_ptr[b + 1] - P.row_ptr[b] + 1});
           }
       };
       add(sysb[n]);
@@ -187,19 +195,19 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     const int x = (int)(std::min_element(load.begin(), load.end()) -
                         load.begin());
     q[x].push_back(it.w);
-    load[x] += it.cost + 1;
+    load[x] += it.cost;
   }
   int64_t rest = 0;
-  for (const Item& it : other_items) rest += it.cost + 1;
+  for (const Item& it : other_items) rest += it.cost;
   const int64_t all = rest + std::accumulate(load.begin(), load.end(),
                                              int64_t(0));
   const int64_t target = (all + kXcds - 1) / kXcds;
   size_t pos = 0;
   for (int x = 0; x < kXcds; ++x) {
     while (pos < other_items.size() &&
-           (x == kXcds - 1 || load[x] + other_items[pos].cost + 1 <= target)) {
+           (x == kXcds - 1 || load[x] + other_items[pos].cost <= target)) {
       q[x].push_back(other_items[pos].w);
-      load[x] += other_items[pos].cost + 1;
+      load[x] += other_items[pos].cost;
       ++pos;
     }
   }
@@ -218,7 +226,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
       if (r < q[x].size()) {
         P.items.push_back(q[x][r]);
       } else {
-        WorkItem pad{-1, 0, 0, 0, -1, 0, 0, 0};
+        WorkItem pad{-1, 0, 0, 0, 0, -1, 0, 0};
         P.items.push_back(pad);
       }
     }

@@ -33,17 +33,23 @@ struct SeqDesc {
   int32_t tile0, n_tiles;               // query-token tiles (TextTile index)
 };
 
-// One attention work item: a query block, one query head, a contiguous run
-// of that block's CSR row. Items of split query-token rows carry a slot.
+// Query heads per work item. The heads of one item share a kv head, so each
+// key/value tile staged in LDS serves all of them.
+constexpr int kHeadsPerItem = 2;
+
+// One attention work item: a query block, up to kHeadsPerItem consecutive
+// query heads of one kv head, and a contiguous run of the block's CSR row.
+// Items of split query-token rows carry the first head's partial slot; head
+// head+i uses slot + i*nch.
 struct WorkItem {
   int32_t qblock;    // -1: padding, exits immediately
-  int32_t head;
+  int32_t head;      // first query head
+  int32_t nheads;    // 1..kHeadsPerItem
   int32_t kb_begin;  // CSR positions [kb_begin, kb_end)
   int32_t kb_end;
-  int32_t slot;      // -1 for visual/system rows; else partial-result slot
+  int32_t slot;      // -1 for visual/system rows; else first head's slot
   int32_t seq;       // video of the query block
-  int32_t chunk;     // chunk index within its row (query-token rows)
-  int32_t pad;
+  int32_t nch;       // chunks of this query-token row (0 for other rows)
 };
 
 // A query-token block and its chunk slots: slot(h, c) = slot0 + h*n_chunks + c.
@@ -86,7 +92,7 @@ std::string build_plan(const Layout& layout, const Rule& rule, int32_t hq,
 
 // Number of hardware queues the launch order interleaves (one per XCD).
 constexpr int kXcds = 8;
-// Concurrent work-item slots the split heuristic aims to fill.
-constexpr int kTargetSlots = 1024;
+// Concurrent work items the split heuristic aims to fill (256 CUs x 2).
+constexpr int kTargetSlots = 512;
 
 }  // namespace evisel

@@ -85,31 +85,36 @@ def test_workload_plans(lib, cid):
 
 
 def _check_work(m, csr, hq):
+    """Every (query block, head) is covered exactly once by contiguous runs of
+    its CSR row; heads of an item share a kv head; query-token items use
+    distinct slots that exactly fill [0, n_chunk_slots)."""
     wk = ev.mask_export_work(m)
-    region = csr["region"]
-    rp = csr["row_ptr"]
-    seen = {}
-    slots = set()
-    for qb, h, a, e, s in zip(wk["qblock"], wk["head"], wk["kb_begin"],
-                              wk["kb_end"], wk["slot"]):
+    region, rp = csr["region"], csr["row_ptr"]
+    group = hq // m.stats["hkv"]
+    seen, text_items = {}, []
+    for qb, h0, nh, a, e, s in zip(wk["qblock"], wk["head"], wk["nheads"],
+                                   wk["kb_begin"], wk["kb_end"], wk["slot"]):
         if qb < 0:
             continue
         assert rp[qb] <= a < e <= rp[qb + 1]
-        seen.setdefault((int(qb), int(h)), []).append((int(a), int(e)))
+        assert 1 <= nh <= 2 and h0 // group == (h0 + nh - 1) // group
+        for i in range(nh):
+            seen.setdefault((int(qb), int(h0 + i)), []).append((int(a), int(e)))
         if region[qb] == 2:
-            assert s >= 0 and s not in slots
-            slots.add(int(s))
+            text_items.append((int(qb), int(h0), int(nh), int(s)))
         else:
             assert s == -1 and (a, e) == (rp[qb], rp[qb + 1])
-    nb = len(region)
-    assert len(seen) == nb * hq
+    assert len(seen) == len(region) * hq
     for (qb, h), runs in seen.items():
         runs.sort()
         assert runs[0][0] == rp[qb] and runs[-1][1] == rp[qb + 1]
         for (a0, e0), (a1, e1) in zip(runs, runs[1:]):
             assert e0 == a1
-    assert len(slots) == m.stats["n_chunk_slots"]
-    assert slots == set(range(m.stats["n_chunk_slots"]))
+    slots = []
+    for qb, h0, nh, s in text_items:
+        nch = len(seen[(qb, h0)])
+        slots.extend(s + i * nch for i in range(nh))
+    assert sorted(slots) == list(range(m.stats["n_chunk_slots"]))
 
 
 def _status(fn):
