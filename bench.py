@@ -30,6 +30,24 @@ PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 flop/clk (dense)
 PEAK_HBM_GBS = 8000.0
 
 
+def measured_traffic():
+    """HBM bytes per attention launch from the committed counter summary,
+    or None when the attention source changed since it was measured."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2608_05780_amd", "csrc", "attn.hip")
+    summ = os.path.join(ROOT, "profiles", "attn_kernel_16k28L_hbm_counters.md")
+    try:
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        for line in open(summ):
+            if line.startswith("traffic_per_launch"):
+                kv = dict(x.split("=") for x in line.split()[1:])
+                if kv["attn_source_sha256"] == sha:
+                    return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
+    except (OSError, KeyError, ValueError):
+        pass
+    return None
+
+
 def _world():
     return int(os.environ.get("WORLD_SIZE", "1")), int(os.environ.get("RANK",
                                                                       "0"))
@@ -192,7 +210,8 @@ def main():
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "mfma", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic() if args.config == 3 else None,
                      "kernel": "attn_kernel<Bf16Path<128>>",
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms},

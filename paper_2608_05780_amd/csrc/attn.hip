@@ -84,37 +84,72 @@ __device__ __forceinline__ float pair_max(float x) {
 }
 
 // 16-byte chunk swizzles of a 64-row LDS tile: physical chunk = logical
-// chunk ^ swz(row).
+// chunk ^ swz(row), RC chunks per row. They keep the operand reads free of
+// bank conflicts whether the LDS serves 128 or 256 bytes per pass:
+//   K (ds_read_b128, lane = key): 16 consecutive keys hit 16 distinct
+//     chunk positions (8 when a row has only 8 chunks);
+//   V (ds_read_b64_tr_b16): the 4 rows a 16-lane group addresses take the
+//     XOR masks 0, 6, 10, 12, whose bits 1-2 and bits 2-3 are both distinct,
+//     so 2-chunk (128 B) and 4-chunk (256 B) row slices never collide.
 enum Swz { kSwzK = 0, kSwzV = 1, kSwzNone = 2 };
-template <int SWZ>
+template <int SWZ, int RC>
 __device__ __forceinline__ int swz(int row) {
-  return SWZ == kSwzK ? (row & 7) : SWZ == kSwzV ? ((row & 3) << 1) : 0;
+  if (SWZ == kSwzK) return row & (RC >= 16 ? 15 : 7);
+  if (SWZ == kSwzV) return ((0xCA60 >> (4 * (row & 3))) & 15) & (RC - 1);
+  return 0;
 }
 
-// Issues the loads of one 64-key tile of a [S][H][D] tensor (head kvh) into
-// LDS: every thread fetches 64*RC/256 chunks of 16 bytes; a wavefront's load
-// fills 64 consecutive 16-byte LDS slots. Rows past klen re-read the last
-// valid row (finite values; they are masked to zero probability).
+// Loads of one 64-key tile of a [S][H][D] tensor into LDS: every thread
+// fetches N = 64*RC/256 chunks of 16 bytes and a wavefront's load fills 64
+// consecutive 16-byte LDS slots. The (row, chunk) a lane fetches is fixed,
+// so its byte offset from the tile's first row is computed once; per tile
+// the address is a wave-uniform base plus that offset. Rows past klen
+// re-read row klen-1 (finite values; they get zero probability).
 template <typename T, int D, int SWZ>
-__device__ __forceinline__ void issue_tile(EV_LDS char* buf, const T* src,
-                                           int kstart, int klen, int kvh,
-                                           int hkv, int wave, int lane) {
-  constexpr int RC = D * (int)sizeof(T) / 16;
-  constexpr int N = kTile * RC / kThreads;
+struct TileLoader {
+  static constexpr int RC = D * (int)sizeof(T) / 16;
+  static constexpr int N = kTile * RC / kThreads;
+  static constexpr int RSTEP = 64 / RC;   // row step between loads i, i+1
+  uint32_t off[N];    // byte offset of this lane's chunk for a full tile
+  int row0;           // row of load 0 (load i fetches row row0 + i*RSTEP)
+  uint32_t rowbytes;  // bytes between consecutive tokens (hkv * D * sizeof T)
+
+  __device__ void init(int hkv, int wave, int lane) {
+    rowbytes = (uint32_t)hkv * D * sizeof(T);
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
-    const int slot = (wave * N + i) * 64 + lane;
-    const int row = slot / RC;
-    const int ch = (slot % RC) ^ swz<SWZ>(row);
-    const int srow = row < klen ? row : klen - 1;
-    const char* g =
-        (const char*)(src + ((size_t)(kstart + srow) * hkv + kvh) * D) +
-        ch * 16;
-    __builtin_amdgcn_global_load_lds((const void*)g,
-                                     (EV_LDS void*)(buf + (wave * N + i) * 1024),
-                                     16, 0, 0);
+    for (int i = 0; i < N; ++i) {
+      const int slot = (wave * N + i) * 64 + lane;
+      const int r = slot / RC;
+      const int ch = (slot % RC) ^ swz<SWZ, RC>(r);
+      if (i == 0) row0 = r;
+      off[i] = (uint32_t)r * rowbytes + (uint32_t)ch * 16;
+    }
   }
-}
+
+  __device__ void issue(EV_LDS char* buf, const T* src, int kstart, int klen,
+                        int kvh, int wave) const {
+    const char* base =
+        (const char*)src + ((size_t)kstart * rowbytes + (size_t)kvh * D *
+                                                            sizeof(T));
+    if (klen == kTile) {
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(base + off[i]),
+            (EV_LDS void*)(buf + (wave * N + i) * 1024), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int r = row0 + i * RSTEP;
+        const uint32_t over =
+            r >= klen ? (uint32_t)(r - (klen - 1)) * rowbytes : 0u;
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(base + (off[i] - over)),
+            (EV_LDS void*)(buf + (wave * N + i) * 1024), 16, 0, 0);
+      }
+    }
+  }
+};
 
 // ---------------------------------------------------------------------------
 // bf16 operands.
@@ -145,7 +180,7 @@ struct Bf16Path {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const int key = 32 * c + l32;
-        const int ch = (2 * kk + g) ^ swz<kSwzK>(key);
+        const int ch = (2 * kk + g) ^ swz<kSwzK, RC>(key);
         const bf16x8 kf = *(const EV_LDS bf16x8*)(kt + (key * RC + ch) * 16);
         s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf.x[kk], s[c], 0,
                                                         0, 0);
@@ -163,7 +198,7 @@ struct Bf16Path {
   __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
                             const f32x16 (&p)[2], int lane) {
     const int j = lane & 15, q16 = lane >> 4, g = lane >> 5;
-    const int sw = (j >> 2) << 1;   // swz<kSwzV>(row): row % 4 == j / 4
+    const int sw = swz<kSwzV, RC>(j >> 2);   // row % 4 == j / 4 below
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
 #pragma unroll
@@ -231,7 +266,7 @@ struct F32Path {
       const int key = 32 * c + l32;
 #pragma unroll
       for (int u = 0; u < D / 8; ++u) {
-        const int ch = (g * D / 8 + u) ^ swz<kSwzK>(key);
+        const int ch = (g * D / 8 + u) ^ swz<kSwzK, RC>(key);
         const f32x4 kf = *(const EV_LDS f32x4*)(kt + (key * RC + ch) * 16);
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
@@ -277,7 +312,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 
   const WorkItem it = pl.items[blockIdx.x];
   if (it.qblock < 0) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
   const int l32 = lane & 31, g = lane >> 5;
   const int hsub = wave >> 1;
   const bool active = hsub < it.nheads;
@@ -301,30 +337,23 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) o[i] = f32x16{};
 
-  BlockDesc kb = pl.blocks[pl.col[it.kb_begin]];
-  issue_tile<T, D, kSwzK>(lds, kg, kb.start, kb.len, kvh, pl.hkv, wave, lane);
-  issue_tile<T, D, VSWZ>(lds + TB, vg, kb.start, kb.len, kvh, pl.hkv, wave,
-                         lane);
+  TileLoader<T, D, kSwzK> kload;
+  TileLoader<T, D, VSWZ> vload;
+  kload.init(pl.hkv, wave, lane);
+  vload.init(pl.hkv, wave, lane);
+  // LDS layout: [K0 | K1 | V0 | V1], tile t in buffers t % 2.
+  EV_LDS char* const kbuf0 = lds;
+  EV_LDS char* const vbuf0 = lds + 2 * TB;
+  auto kbuf = [&](int t) { return kbuf0 + (t & 1) * TB; };
+  auto vbuf = [&](int t) { return vbuf0 + (t & 1) * TB; };
+  const int b0 = it.kb_begin;
 
-  for (int j = 0; j < n; ++j) {
-    const BlockDesc cur = kb;
-    const EV_LDS char* kt = lds + (j & 1) * 2 * TB;
-    const EV_LDS char* vt = kt + TB;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (j + 1 < n) {
-      kb = pl.blocks[pl.col[it.kb_begin + j + 1]];
-      EV_LDS char* nk = lds + ((j + 1) & 1) * 2 * TB;
-      issue_tile<T, D, kSwzK>(nk, kg, kb.start, kb.len, kvh, pl.hkv, wave,
-                              lane);
-      issue_tile<T, D, VSWZ>(nk + TB, vg, kb.start, kb.len, kvh, pl.hkv,
-                             wave, lane);
-    }
-    if (!active) continue;
-
-    f32x16 s[2] = {f32x16{}, f32x16{}};
-    P::qk(s, kt, qf, l32, g);
-
+  // Per tile, in three parts:
+  //   pre:  causal / length mask (only on tiles that need it), row max and
+  //         the (rare) lazy rescale of the accumulators;
+  //   main: p = exp2(s * scale - m_ref) in place, row-sum partial;
+  //   post: evidence partials of query-token rows, then O^T += V^T P^T.
+  auto tile_pre = [&](f32x16 (&s)[2], const BlockDesc& cur) {
     if (cur.len < kTile || cur.start + cur.len - 1 > qb.start) {
 #pragma unroll
       for (int c = 0; c < 2; ++c)
@@ -334,7 +363,6 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
           if (kl >= cur.len || cur.start + kl > qpos) s[c][r] = neg_inf();
         }
     }
-
     float mx = neg_inf();
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -351,6 +379,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       for (int i = 0; i < D / 32; ++i) o[i] *= alpha;
       m_ref = need ? m_new : m_ref;
     }
+  };
+  auto tile_main = [&](f32x16 (&s)[2]) -> float {
     const float mu = m_ref == neg_inf() ? 0.f : m_ref;
     float ts = 0.f;
 #pragma unroll
@@ -362,8 +392,18 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         ts += p;
       }
     l_part += ts;
-
+    return ts;
+  };
+  // query-token rows: this video's offsets (read once, outside the loop)
+  SeqDesc sq{};
+  if (is_text) sq = pl.seqs[it.seq];
+  const int trow = qb.aux + qrow - sq.textrow0;
+  float* const seg_row = ws.seg + (size_t)h * pl.segtot + sq.segbase +
+                         (size_t)trow * sq.n_frames - sq.frame0;
+  auto tile_post = [&](f32x16 (&s)[2], const BlockDesc& cur, float ts,
+                       const EV_LDS char* vt) {
     if (is_text) {
+      const float mu = m_ref == neg_inf() ? 0.f : m_ref;
       if (cur.region == kVis) {
         // per 8-key group partial sums, completed across the lane pair
         float g8[8];
@@ -377,10 +417,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         for (int q = 0; q < 8; ++q) g8[q] = pair_sum(g8[q]);
         const int lg = __builtin_ctz((unsigned)pl.Nv) - 3;  // log2(N_v / 8)
         const int nseg = kTile / pl.Nv;
-        const SeqDesc sq = pl.seqs[it.seq];
-        const int trow = qb.aux + qrow - sq.textrow0;
-        float* dst = ws.seg + (size_t)h * pl.segtot + sq.segbase +
-                     (size_t)trow * sq.n_frames + (cur.aux - sq.frame0);
+        float* dst = seg_row + cur.aux;
         for (int si = 0; si < nseg; ++si) {
           float t = 0.f;
 #pragma unroll
@@ -392,8 +429,56 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         nv_part += ts;
       }
     }
-
     P::pv(o, vt, s, lane);
+  };
+
+  // Descriptors of this item's key tiles, 64 at a time: lane t holds the
+  // BlockDesc of tile 64*batch + t, and the loop reads tile j's with
+  // v_readlane. (Loading them per tile would put two dependent global round
+  // trips in front of every tile's K/V loads.)
+  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0;
+  auto load_batch = [&](int batch) {
+    const int t = batch * 64 + lane;
+    if (t < n) {
+      const BlockDesc bd = pl.blocks[pl.col[b0 + t]];
+      dsc_start = bd.start;
+      dsc_len = bd.len;
+      dsc_region = bd.region;
+      dsc_aux = bd.aux;
+    }
+  };
+  auto desc = [&](int t) {
+    const int l = t & 63;
+    BlockDesc d;
+    d.start = __builtin_amdgcn_readlane(dsc_start, l);
+    d.len = __builtin_amdgcn_readlane(dsc_len, l);
+    d.region = __builtin_amdgcn_readlane(dsc_region, l);
+    d.aux = __builtin_amdgcn_readlane(dsc_aux, l);
+    return d;
+  };
+
+  // Tile j+1 streams into the other buffer pair while tile j is computed.
+  load_batch(0);
+  BlockDesc kb = desc(0);
+  kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
+  vload.issue(vbuf(0), vg, kb.start, kb.len, kvh, wave);
+  for (int j = 0; j < n; ++j) {
+    const BlockDesc cur = kb;
+    if (((j + 1) & 63) == 0 && j + 1 < n) load_batch((j + 1) >> 6);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (j + 1 < n) {
+      kb = desc(j + 1);
+      kload.issue(kbuf(j + 1), kg, kb.start, kb.len, kvh, wave);
+      vload.issue(vbuf(j + 1), vg, kb.start, kb.len, kvh, wave);
+    }
+    if (active) {
+      f32x16 s[2] = {f32x16{}, f32x16{}};
+      P::qk(s, kbuf(j), qf, l32, g);
+      tile_pre(s, cur);
+      const float ts = tile_main(s);
+      tile_post(s, cur, ts, vbuf(j));
+    }
   }
   if (!active) return;
 
@@ -437,18 +522,19 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 
 // ---------------------------------------------------------------------------
 // Merge the chunks of a query-token tile: one work-group per (tile, head),
-// four threads per row. Also leaves the rows' log2 LSE for the evidence
+// eight threads per row. Also leaves the rows' log2 LSE for the evidence
 // reduction and the tile's non-visual mass.
+constexpr int kCombineThreads = 512;
+
 template <int D, bool F32>
-__global__ __launch_bounds__(256) void combine_kernel(const DevPlan pl,
-                                                      const Workspace ws,
-                                                      const AttnCall ac) {
-  constexpr int DP = D / 4;
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(
+    const DevPlan pl, const Workspace ws, const AttnCall ac) {
+  constexpr int DP = D / 8;
   __shared__ float red[kTile];
   const TextTile tt = pl.tiles[blockIdx.x];
   const int h = blockIdx.y;
   const BlockDesc qb = pl.blocks[tt.qblock];
-  const int tid = threadIdx.x, r = tid >> 2, part = tid & 3;
+  const int tid = threadIdx.x, r = tid >> 3, part = tid & 7;
   float nvmass = 0.f;
   if (r < qb.len) {
     const int slot0 = tt.slot0 + h * tt.n_chunks;
@@ -527,7 +613,7 @@ hipError_t launch_attention(const DevPlan& p, const Workspace& w,
 hipError_t launch_combine(const DevPlan& p, const Workspace& w,
                           const AttnCall& c, hipStream_t s) {
   if (p.n_tiles == 0) return hipSuccess;
-  dim3 grid(p.n_tiles, p.hq), block(256);
+  dim3 grid(p.n_tiles, p.hq), block(kCombineThreads);
   if (c.fp32) {
     if (c.d == 64)
       combine_kernel<64, true><<<grid, block, 0, s>>>(p, w, c);

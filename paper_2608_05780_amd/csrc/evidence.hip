@@ -3,11 +3,13 @@
 // evidence_kernel: E[h, f] = sum over the query rows r of f's video of
 //   exp2(seg[h, r, f] - lse2[h, r]), i.e. each row's softmax mass on frame f
 //   (the query-frame cue of Evidence Decomposition, kept as a raw sum over the
-//   query rows). One thread per (head, frame), rows in a fixed order, one
-//   store per output: no atomics, bitwise reproducible. Adjacent threads read
-//   adjacent frames of the same row, so every load is coalesced.
+//   query rows). A work-group takes 64 frames of one head; 16 row groups sum
+//   strided rows and are added in a fixed order in LDS, one store per
+//   output: no atomics, bitwise reproducible. Adjacent threads read adjacent
+//   frames of the same row, so every load is coalesced.
 // frame_mean_kernel: E_qf[l, t] = sum_h E[l, h, t] / (Hq * n_text) and the
-//   mean over layers (heads averaged per layer, layer kept).
+//   mean over layers (heads averaged per layer, layer kept); 32 frames x 32
+//   layer groups per work-group, layers added in a fixed order.
 // topk_kernel: per video, rank r(t) = #{t' : e(t') > e(t) or (e(t') == e(t)
 //   and t' < t)}; frames with r(t) < k land at topk[offset + r(t)]. Ranks of a
 //   strict total order are a permutation, so every slot gets one writer.
@@ -20,24 +22,35 @@ __device__ __forceinline__ float exp2_(float x) {
   return __builtin_amdgcn_exp2f(x);
 }
 
-__global__ __launch_bounds__(256) void evidence_kernel(const DevPlan pl,
-                                                       const Workspace ws,
-                                                       float* __restrict__ ev,
-                                                       float* __restrict__ tm) {
+constexpr int kEvFrames = 64, kEvRows = 16;
+
+__global__ __launch_bounds__(kEvFrames * kEvRows) void evidence_kernel(
+    const DevPlan pl, const Workspace ws, float* __restrict__ ev,
+    float* __restrict__ tm) {
+  __shared__ float red[kEvRows][kEvFrames];
   const int h = blockIdx.y;
-  const int f = blockIdx.x * 256 + threadIdx.x;
+  const int fl = threadIdx.x % kEvFrames, rg = threadIdx.x / kEvFrames;
+  const int f = blockIdx.x * kEvFrames + fl;
+  float acc = 0.f;
   if (f < pl.T) {
     const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
     const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
                        (f - sq.frame0);
     const float* l2 = ws.lse2t + (size_t)h * pl.n_text_rows + sq.textrow0;
-    float acc = 0.f;
-    for (int r = 0; r < sq.n_text; ++r)
+#pragma unroll 4
+    for (int r = rg; r < sq.n_text; r += kEvRows)
       acc += exp2_(src[(size_t)r * sq.n_frames] - l2[r]);
-    ev[(size_t)h * pl.T + f] = acc;
+  }
+  red[rg][fl] = acc;
+  __syncthreads();
+  if (rg == 0 && f < pl.T) {
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < kEvRows; ++i) t += red[i][fl];
+    ev[(size_t)h * pl.T + f] = t;
   }
   if (tm && blockIdx.x == 0) {
-    for (int n = threadIdx.x; n < pl.n_seq; n += 256) {
+    for (int n = threadIdx.x; n < pl.n_seq; n += kEvFrames * kEvRows) {
       const SeqDesc sq = pl.seqs[n];
       float t = 0.f;
       for (int i = 0; i < sq.n_tiles; ++i)
@@ -47,23 +60,36 @@ __global__ __launch_bounds__(256) void evidence_kernel(const DevPlan pl,
   }
 }
 
-__global__ __launch_bounds__(256) void frame_mean_kernel(
+constexpr int kFmFrames = 32, kFmLayers = 32;
+
+__global__ __launch_bounds__(kFmFrames * kFmLayers) void frame_mean_kernel(
     const DevPlan pl, const float* __restrict__ ev, int n_layers,
     float* __restrict__ e_layer, float* __restrict__ e_qf) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= pl.T) return;
-  const SeqDesc sq = pl.seqs[pl.frame_seq[t]];
-  const float denom = (float)pl.hq * (float)sq.n_text;
-  float pooled = 0.f;
-  for (int l = 0; l < n_layers; ++l) {
-    float s = 0.f;
-    for (int h = 0; h < pl.hq; ++h)
-      s += ev[((size_t)l * pl.hq + h) * pl.T + t];
-    const float v = s / denom;
-    if (e_layer) e_layer[(size_t)l * pl.T + t] = v;
-    pooled += v;
+  __shared__ float red[kFmLayers][kFmFrames];
+  const int tl = threadIdx.x % kFmFrames, lg = threadIdx.x / kFmFrames;
+  const int t = blockIdx.x * kFmFrames + tl;
+  float part = 0.f;
+  if (t < pl.T) {
+    const SeqDesc sq = pl.seqs[pl.frame_seq[t]];
+    const float denom = (float)pl.hq * (float)sq.n_text;
+    for (int l = lg; l < n_layers; l += kFmLayers) {
+      float s = 0.f;
+#pragma unroll 4
+      for (int h = 0; h < pl.hq; ++h)
+        s += ev[((size_t)l * pl.hq + h) * pl.T + t];
+      const float v = s / denom;
+      if (e_layer) e_layer[(size_t)l * pl.T + t] = v;
+      part += v;
+    }
   }
-  e_qf[t] = pooled / (float)n_layers;
+  red[lg][tl] = part;
+  __syncthreads();
+  if (lg == 0 && t < pl.T) {
+    float pooled = 0.f;
+#pragma unroll
+    for (int i = 0; i < kFmLayers; ++i) pooled += red[i][tl];
+    e_qf[t] = pooled / (float)n_layers;
+  }
 }
 
 constexpr int kTopkThreads = 1024;
@@ -106,7 +132,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
 
 hipError_t launch_evidence(const DevPlan& p, const Workspace& w, float* ev,
                            float* tm, hipStream_t s) {
-  dim3 grid((p.T + 255) / 256, p.hq), block(256);
+  dim3 grid((p.T + kEvFrames - 1) / kEvFrames, p.hq),
+      block(kEvFrames * kEvRows);
   evidence_kernel<<<grid, block, 0, s>>>(p, w, ev, tm);
   return hipGetLastError();
 }
@@ -115,7 +142,8 @@ hipError_t launch_frame_evidence(const DevPlan& p, const float* evidence,
                                  int32_t n_layers, float* e_qf_layer,
                                  float* e_qf, const int32_t* k_per_seq,
                                  int32_t* topk, hipStream_t s) {
-  frame_mean_kernel<<<dim3((p.T + 255) / 256), dim3(256), 0, s>>>(
+  frame_mean_kernel<<<dim3((p.T + kFmFrames - 1) / kFmFrames),
+                      dim3(kFmFrames * kFmLayers), 0, s>>>(
       p, evidence, n_layers, e_qf_layer, e_qf);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !k_per_seq) return e;

@@ -92,7 +92,7 @@ std::string build_plan(const Layout& layout, const Rule& rule, int32_t hq,
 
 // Number of hardware queues the launch order interleaves (one per XCD).
 constexpr int kXcds = 8;
-// Concurrent work items the split heuristic aims to fill (256 CUs x 2).
+// Concurrent work items the split heuristic aims to fill (256 CUs x 1).
 constexpr int kTargetSlots = 512;
 
 }  // namespace evisel

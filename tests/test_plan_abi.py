@@ -97,7 +97,7 @@ def _check_work(m, csr, hq):
         if qb < 0:
             continue
         assert rp[qb] <= a < e <= rp[qb + 1]
-        assert 1 <= nh <= 2 and h0 // group == (h0 + nh - 1) // group
+        assert 1 <= nh <= 4 and h0 // group == (h0 + nh - 1) // group
         for i in range(nh):
             seen.setdefault((int(qb), int(h0 + i)), []).append((int(a), int(e)))
         if region[qb] == 2:
