@@ -21,11 +21,16 @@ What it computes (each function cites the passage it follows):
                    top-k frames.
 * ``blocks``    -- the block-level active set implied by the token predicate.
 * ``brute``     -- pure-Python loops over tiny inputs (an independent pin).
+* ``topp``      -- the paper's adaptive top-p block retention (mean-key block
+                   representative, block affinity over the history H_i,
+                   softmax, smallest subset reaching tau_p) and the attention
+                   and evidence it induces (appendix, "Detailed Sparse
+                   Prefilling").
 
 Parity pins live in ``tests/`` (brute force, closed forms, a library attention
 routine, invariants, planted ranking). No function here is "parity unpinned".
 """
-from . import layout, attention, aggregate, blocks, brute  # noqa: F401
+from . import layout, attention, aggregate, blocks, brute, topp  # noqa: F401
 from .layout import Layout, Rule  # noqa: F401
 from .attention import run_layer, attend  # noqa: F401
 from .aggregate import frame_evidence, topk_per_video  # noqa: F401
