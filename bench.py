@@ -16,6 +16,13 @@ Prints one JSON line: probe tokens/s (value), ms per step, the attention
 kernel's roofline against the bf16 MFMA peak (active-block FLOPs over the
 kernel's HIP-event time, measured over the timed region), and the fp64 CPU
 oracle's throughput on a bounded sample (one full layer) as a baseline.
+
+``--tau-p P`` runs the same workload under the paper's adaptive top-p
+retention instead of the static rule: every layer first selects each row's
+history blocks on the GPU (that time is part of the step), and the
+attention's active-block FLOPs are those of the key tiles actually computed
+(after dropping tiles no row of a work item retained), counted per layer
+from the retention bits after the timed region.
 """
 import argparse
 import json
@@ -46,6 +53,48 @@ def measured_traffic():
     except (OSError, KeyError, ValueError):
         pass
     return None
+
+
+def topp_computed_pairs(ev, mask, w, qs, kks, ws):
+    """Key tiles the top-p attention computes per layer (mean over
+    layers), summed over query heads, and the mean fraction of its history
+    a row retains. Recomputes each layer's retention (same kernels)."""
+    import numpy as np
+    import torch
+    st = mask.stats
+    nb, W = st["n_blocks"], st["hist_words"]
+    ex = ev.mask_export(mask)
+    wk = ev.mask_export_work(mask)
+    col, rp = ex["col"], ex["row_ptr"]
+    # local history index of every block (-1: system prefix)
+    local = np.full(nb, -1, np.int64)
+    for n in np.unique(ex["video"]):
+        ids = np.nonzero((ex["video"] == n) & (ex["region"] != 0))[0]
+        local[ids] = np.arange(ids.size)
+    rb = torch.empty((w.hq, nb, W, 64), dtype=torch.int32, device="cuda")
+    ub = torch.empty((w.hq, nb, W), dtype=torch.int32, device="cuda")
+    total, kept, hist = 0.0, 0.0, 0.0
+    for l in range(len(qs)):
+        ev.select_blocks(mask, qs[l], kks[l], rb, ub, ws,
+                         softmax_scale=w.softmax_scale)
+        u = ub.cpu().numpy().view(np.uint32)
+        for qb, h0, nh, a, e in zip(wk["qblock"], wk["head"], wk["nheads"],
+                                    wk["kb_begin"], wk["kb_end"]):
+            if qb < 0:
+                continue
+            c = col[a:e]
+            loc = local[c]
+            always = (loc < 0) | (c == qb)
+            lc = np.maximum(loc, 0)
+            word = np.bitwise_or.reduce(u[h0:h0 + nh, qb][:, lc // 32], axis=0)
+            keep = always | (((word >> (lc % 32).astype(np.uint32)) & 1) > 0)
+            total += float(keep.sum()) * nh
+        bits = rb.cpu().numpy().view(np.uint32)
+        pc = np.unpackbits(bits.view(np.uint8)).reshape(-1).sum()
+        kept += float(pc)
+        lens = ex["len"].astype(np.int64)
+        hist += float((np.maximum(local, 0) * lens).sum() * w.hq)
+    return total / len(qs), kept / max(hist, 1.0)
 
 
 def _world():
@@ -89,6 +138,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tau-p", type=float, default=0.0,
+                    help="adaptive top-p retention threshold (0: the "
+                         "workload's static rule)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes "
                          "(3 times), to scale HBM byte counters")
@@ -119,7 +171,8 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 3}))
         return
     ev.load()
-    w = wl.get(args.config)
+    w = wl.get(args.config, tau_p=args.tau_p) if args.tau_p > 0 else \
+        wl.get(args.config)
     L = w.n_layers
     ns, nf, nt = wl.layout_arrays(w, args.seed)
     _, core, _ = wl.plant_table(w, args.seed)
@@ -130,7 +183,8 @@ def main():
         off += int(F)
 
     mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
-                               w.sink_blocks, w.window, w.hq, w.hkv, n_sys=ns)
+                               w.sink_blocks, w.window, w.hq, w.hkv, n_sys=ns,
+                               tau_p=w.tau_p)
     st = mask.stats
     S, T = st["n_tokens"], st["n_frames_total"]
     print(f"# {w.name}: S={S} T={T} active pairs/head/layer="
@@ -183,7 +237,12 @@ def main():
 
     found = sorted(topk[:sum(ks)].cpu().numpy().tolist())
     planted_ok = found == sorted(core.tolist())
-    flop_layer = 4.0 * w.block * w.block * w.d * w.hq * st["n_active_pairs"]
+    tile_flop = 4.0 * w.block * w.block * w.d
+    if w.tau_p > 0:
+        pairs, kept_frac = topp_computed_pairs(ev, mask, w, qs, kks, ws)
+        flop_layer = tile_flop * pairs
+    else:
+        flop_layer = tile_flop * w.hq * st["n_active_pairs"]
     attn_ms = prof["attention_ms"] / max(1, prof["calls"])
     achieved = flop_layer / (attn_ms * 1e-3) / 1e12
     ev_ms = prof["evidence_ms"] / max(1, prof["calls"])
@@ -216,12 +275,22 @@ def main():
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms},
         "kernels_ms_per_layer": {
+            "retention": prof["select_ms"] / max(1, prof["calls"]),
             "attention": attn_ms,
             "combine": prof["combine_ms"] / max(1, prof["calls"]),
             "evidence": ev_ms},
         "evidence_reduce_GBps": ev_bytes / (ev_ms * 1e-3) / 1e9,
         "topk_planted_recovered": planted_ok,
     }
+    if w.tau_p > 0:
+        rec["config"]["tau_p"] = w.tau_p
+        rec["config"]["sink_blocks"] = rec["config"]["window"] = None
+        rec["roofline"]["kernel"] = "attn_kernel<Bf16Path<128>, top-p>"
+        rec["topp"] = {"computed_tile_pairs_per_layer": flop_layer / tile_flop,
+                       "candidate_tile_pairs_per_layer":
+                           float(w.hq * st["n_active_pairs"]),
+                       "row_retained_fraction": kept_frac}
+        args.no_cpu_baseline = True    # the oracle baseline is the static one
     if not args.no_cpu_baseline and rank == 0:
         print("# timing the CPU oracle on one layer ...", file=sys.stderr,
               flush=True)

@@ -58,17 +58,33 @@ typedef struct {
   int32_t tokens_per_frame; /* N_v */
 } evisel_layout;
 
-/* Static block-sparse rule (appendix: frame-aligned blocks of B tokens per
- * region, the last block of a region may be short). A visual query token in
- * visual block b sees visual blocks [0, sink_blocks), [b - window, b - 1]
- * and its own block b up to itself; window = -1 makes every preceding visual
- * block visible (plain causal attention). A query (text) token sees every
- * visual block and the query tokens up to itself. System-prefix tokens are
- * visible to every later token of their video. Videos never see each other. */
+/* Block-sparse rule (appendix: frame-aligned blocks of B tokens per region,
+ * the last block of a region may be short). System-prefix tokens are visible
+ * to every later token of their video; a token always sees the causal prefix
+ * of its own block; videos never see each other.
+ *
+ * tau_p = 0: static rule. A visual query token in visual block b sees visual
+ * blocks [0, sink_blocks), [b - window, b - 1] and its own block b up to
+ * itself; window = -1 makes every preceding visual block visible (plain
+ * causal attention). A query (text) token sees every visual block and the
+ * query tokens up to itself.
+ *
+ * 0 < tau_p <= 1: the paper's adaptive top-p retention (appendix, mean-key,
+ * affinity and probability equations). A video's selectable blocks are its
+ * visual then query-token blocks, numbered 0, 1, ... in token order (the
+ * "local" index); a token in local block b has the history H = local blocks
+ * 0 .. b-1. Per query head and token, every history block j gets the
+ * affinity g_j = q . kbar_j * softmax_scale, kbar_j the mean of block j's
+ * keys (that head's kv head); p = softmax(g) over H; the token keeps the
+ * smallest set of blocks, taken in decreasing p (equal p: lower index
+ * first), whose total p reaches tau_p, and attends exactly to their tokens,
+ * the system prefix and its own block's causal prefix. sink_blocks and
+ * window are ignored. At most 2048 candidate key blocks per query block. */
 typedef struct {
   int32_t block;       /* B >= 1; the attention kernel supports B = 64 */
   int32_t sink_blocks; /* >= 0 */
   int32_t window;      /* >= 0, or -1 for all-causal */
+  float tau_p;         /* 0 (static rule) or (0, 1] (top-p retention) */
 } evisel_mask_rule;
 
 typedef struct evisel_mask evisel_mask; /* opaque, library-owned */
@@ -83,6 +99,8 @@ typedef struct {
   int64_t n_text_tiles;    /* query-token blocks                        */
   int64_t n_chunk_slots;   /* split query-token work items (all heads)  */
   int32_t hq, hkv, block, tokens_per_frame;
+  int32_t hist_words;      /* W: 32-bit words of one row's history bits   */
+  float tau_p;             /* the rule's tau_p                            */
 } evisel_mask_stats;
 
 /* Builds the block partition, the compact list of active block pairs (CSR,
@@ -129,11 +147,39 @@ evisel_status evisel_mask_export_work(const evisel_mask* mask, int32_t* qblock,
                                       int32_t* kb_begin, int32_t* kb_end,
                                       int32_t* slot);
 
-/* Bytes of device workspace evisel_sparse_prefill needs for head dim d. */
+/* Bytes of device workspace evisel_sparse_prefill (and, for a top-p mask,
+ * evisel_select_blocks) needs for head dim d. */
 size_t evisel_sparse_prefill_workspace(const evisel_mask* mask, int32_t d);
 
-/* One layer of the probe (appendix sparse prefilling restricted to the rule
- * above; evidence per Evidence Decomposition, query-frame cue).
+/* Top-p retention of one layer alone (appendix, mean-key, affinity and
+ * probability equations and the smallest subset reaching tau_p; see
+ * evisel_mask_rule). evisel_sparse_prefill runs the same kernels itself;
+ * this call exposes their result.
+ *   q, k, d, dtype, softmax_scale  as for evisel_sparse_prefill
+ *   row_bits   device uint32 [Hq][n_blocks][W][64]: for query head h, query
+ *              block qb and row r < 64 of the block, bit (j % 32) of word
+ *              j / 32 is set when the row retains local history block j
+ *              (W = hist_words of evisel_mask_info). Rows past the block's
+ *              length, system-prefix blocks and blocks without history are
+ *              all zero.
+ *   block_bits device uint32 [Hq][n_blocks][W]: OR of the block's rows.
+ *   workspace  as for evisel_sparse_prefill (only its mean-key region is
+ *              used)
+ * Probabilities, sums and the cut are computed in fp32; bf16 inputs use
+ * bf16 MFMA with the block means split into two bf16 terms. Deterministic.
+ * Errors: INVALID_ARG (host-only or static mask, NULL or misaligned
+ * pointer), UNSUPPORTED (d, dtype, B), WORKSPACE, HIP. */
+evisel_status evisel_select_blocks(const evisel_mask* mask, const void* q,
+                                   const void* k, int32_t d,
+                                   evisel_dtype dtype, float softmax_scale,
+                                   uint32_t* row_bits, uint32_t* block_bits,
+                                   void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/* One layer of the probe (appendix sparse prefilling under the mask's rule;
+ * evidence per Evidence Decomposition, query-frame cue). With a top-p mask
+ * the call first runs the retention of evisel_select_blocks into the
+ * workspace; key tiles that no row of a work item retained are skipped.
  *   q        device [S, Hq, d]   dtype
  *   k, v     device [S, Hkv, d]  dtype
  *   d        64 or 128; dtype EVISEL_BF16 or EVISEL_FP32
@@ -181,18 +227,19 @@ evisel_status evisel_frame_evidence(const evisel_mask* mask,
                                     const int32_t* k_per_seq,
                                     int32_t* topk_idx, void* stream);
 
-/* Kernel timing, a tracing aid. evisel_profile_begin creates 4 * capacity
+/* Kernel timing, a tracing aid. evisel_profile_begin creates 5 * capacity
  * HIP events on the current device; each later evisel_sparse_prefill call,
- * up to `capacity` calls, records events on its stream before the attention
- * kernel, after it, after the split-row combine and after the evidence
- * reduction. evisel_profile_end waits for those events, writes the summed
- * milliseconds of each kernel and the number of timed calls (any pointer may
- * be NULL) and destroys the events. One session at a time per process; not
- * thread-safe. Errors: INVALID_ARG (capacity < 1, a session already open or
- * none open), NOMEM, HIP. */
+ * up to `capacity` calls, records events on its stream before the top-p
+ * retention (empty for a static mask), before the attention kernel, after
+ * it, after the split-row combine and after the evidence reduction.
+ * evisel_profile_end waits for those events, writes the summed milliseconds
+ * of the four spans into ms[0..3] (retention, attention, combine, evidence)
+ * and the number of timed calls (either pointer may be NULL) and destroys
+ * the events. One session at a time per process; not thread-safe. Errors:
+ * INVALID_ARG (capacity < 1, a session already open or none open), NOMEM,
+ * HIP. */
 evisel_status evisel_profile_begin(int32_t capacity);
-evisel_status evisel_profile_end(double* ms_attention, double* ms_combine,
-                                 double* ms_evidence, int64_t* n_calls);
+evisel_status evisel_profile_end(double* ms, int64_t* n_calls);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* evisel_last_error(void);

@@ -7,6 +7,7 @@ library; the first call does, and raises if it has not been built.
 
 Entry points (same names as the C ABI):
     build_block_mask       layout + rule + head counts -> Mask (plan on device)
+    select_blocks          top-p masks: per-row retained history blocks
     sparse_prefill         one layer: attention output, LSE, evidence slice
     frame_evidence         head/layer aggregation and per-video top-k frames
     sparse_prefill_workspace, mask_info, mask_export, mask_export_work
@@ -19,6 +20,7 @@ from typing import Optional, Sequence
 
 __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "sparse_prefill_workspace", "sparse_prefill", "frame_evidence",
+           "select_blocks", "unpack_row_bits",
            "mask_info", "mask_export", "mask_export_work", "profile_begin",
            "profile_end", "LIB_PATH"]
 
@@ -39,7 +41,7 @@ class _Layout(ctypes.Structure):
 
 class _Rule(ctypes.Structure):
     _fields_ = [("block", ctypes.c_int32), ("sink_blocks", ctypes.c_int32),
-                ("window", ctypes.c_int32)]
+                ("window", ctypes.c_int32), ("tau_p", ctypes.c_float)]
 
 
 class _Stats(ctypes.Structure):
@@ -47,7 +49,8 @@ class _Stats(ctypes.Structure):
         "n_tokens", "n_frames_total", "n_text_rows", "n_blocks",
         "n_active_pairs", "n_work_items", "n_text_tiles", "n_chunk_slots")] + \
         [(n, ctypes.c_int32) for n in ("hq", "hkv", "block",
-                                       "tokens_per_frame")]
+                                       "tokens_per_frame", "hist_words")] + \
+        [("tau_p", ctypes.c_float)]
 
 
 _lib = None
@@ -73,12 +76,16 @@ _SIGS = {
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "evisel_select_blocks": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "evisel_frame_evidence": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "evisel_profile_begin": (ctypes.c_int, [ctypes.c_int32]),
-    "evisel_profile_end": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double)] * 3
-                           + [ctypes.POINTER(ctypes.c_int64)]),
+    "evisel_profile_end": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_int64)]),
     "evisel_last_error": (ctypes.c_char_p, []),
 }
 
@@ -156,14 +163,16 @@ def build_block_mask(n_frames: Sequence[int], n_text: Sequence[int],
                      tokens_per_frame: int, block: int, sink_blocks: int,
                      window: int, hq: int, hkv: int,
                      n_sys: Optional[Sequence[int]] = None, stream=None,
-                     host_only: bool = False) -> Mask:
+                     host_only: bool = False, tau_p: float = 0.0) -> Mask:
+    """``tau_p`` > 0 selects the adaptive top-p retention rule (sink_blocks
+    and window are then ignored)."""
     lib = load()
     ns = list(n_sys) if n_sys is not None else [0] * len(n_frames)
     a_f, a_t, a_s = _arr(n_frames), _arr(n_text), _arr(ns)
     lay = _Layout(len(n_frames), ctypes.cast(a_s, _i32p),
                   ctypes.cast(a_f, _i32p), ctypes.cast(a_t, _i32p),
                   tokens_per_frame)
-    rule = _Rule(block, sink_blocks, window)
+    rule = _Rule(block, sink_blocks, window, float(tau_p))
     h = ctypes.c_void_p()
     if host_only:
         _check(lib.evisel_build_block_mask_host(ctypes.byref(lay),
@@ -240,6 +249,31 @@ def sparse_prefill(mask: Mask, layer: int, n_layers: int, q, k, v, out,
         _stream(stream)))
 
 
+def select_blocks(mask: Mask, q, k, row_bits, block_bits, workspace,
+                  softmax_scale: Optional[float] = None, stream=None):
+    """Top-p retention of one layer. ``row_bits`` is a device int32 tensor
+    [Hq, n_blocks, W, 64], ``block_bits`` [Hq, n_blocks, W] (W =
+    ``mask.stats["hist_words"]``); bit j % 32 of word j // 32 marks local
+    history block j."""
+    d = int(q.shape[-1])
+    scale = float(softmax_scale) if softmax_scale is not None else d ** -0.5
+    _check(load().evisel_select_blocks(
+        mask.handle, _ptr(q), _ptr(k), d, _dtype_code(q), scale,
+        _ptr(row_bits), _ptr(block_bits), _ptr(workspace),
+        0 if workspace is None else workspace.numel() * workspace.element_size(),
+        _stream(stream)))
+
+
+def unpack_row_bits(bits, n_hist: int):
+    """[..., W, 64] int32 words (numpy) -> bool [..., 64, n_hist]."""
+    import numpy as np
+    w = np.ascontiguousarray(bits).view(np.uint32)
+    j = np.arange(n_hist)
+    words = np.take(w, j // 32, axis=-2)              # [..., n_hist, 64]
+    return ((words >> (j % 32).astype(np.uint32)[:, None]) & 1).astype(
+        bool).swapaxes(-1, -2)
+
+
 def frame_evidence(mask: Mask, evidence, n_layers: int, e_qf,
                    e_qf_layer=None, k_per_seq=None, topk=None, stream=None):
     """Head/layer aggregation and top-k. ``k_per_seq`` is a device int32
@@ -256,9 +290,8 @@ def profile_begin(capacity: int):
 
 def profile_end() -> dict:
     """Finish the timing session: summed ms per kernel and the call count."""
-    a, c, e = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    ms = (ctypes.c_double * 4)()
     n = ctypes.c_int64()
-    _check(load().evisel_profile_end(ctypes.byref(a), ctypes.byref(c),
-                                     ctypes.byref(e), ctypes.byref(n)))
-    return {"attention_ms": a.value, "combine_ms": c.value,
-            "evidence_ms": e.value, "calls": n.value}
+    _check(load().evisel_profile_end(ms, ctypes.byref(n)))
+    return {"select_ms": ms[0], "attention_ms": ms[1], "combine_ms": ms[2],
+            "evidence_ms": ms[3], "calls": n.value}

@@ -1,4 +1,5 @@
 // C ABI of libevisel.so: argument validation, plan upload, launches.
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <string>
@@ -51,6 +52,7 @@ evisel_status make_plan(const evisel_layout* layout,
   R.block = rule->block;
   R.sink = rule->sink_blocks;
   R.window = rule->window;
+  R.tau = rule->tau_p;
   evisel_mask* m = new (std::nothrow) evisel_mask();
   if (!m) return fail(EVISEL_ERR_NOMEM, "host allocation failed");
   std::string err;
@@ -63,6 +65,18 @@ evisel_status make_plan(const evisel_layout* layout,
   if (!err.empty()) {
     delete m;
     return fail(EVISEL_ERR_INVALID_ARG, err);
+  }
+  if (R.tau > 0.f) {
+    const evisel::Plan& P = m->plan;
+    const int hmax = P.hist_words * 32;
+    if (P.max_item_candidates > evisel::kMaxItemCandidates ||
+        evisel::select_lds_need(hmax, P.hist_words) > 160 * 1024) {
+      delete m;
+      return fail(EVISEL_ERR_UNSUPPORTED,
+                  "top-p retention supports at most " +
+                      std::to_string(evisel::kMaxItemCandidates) +
+                      " candidate key blocks per query block");
+    }
   }
   *made = m;
   return EVISEL_OK;
@@ -81,7 +95,8 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   std::vector<char> buf;
   const size_t o_blk = put(buf, P.blocks), o_col = put(buf, P.col),
                o_it = put(buf, P.items), o_seq = put(buf, P.seqs),
-               o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq);
+               o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq),
+               o_bl = put(buf, P.blk_local);
   hipError_t e = hipGetDevice(&m->device);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   e = hipMalloc(&m->dev, buf.size());
@@ -101,6 +116,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   dp.seqs = (const evisel::SeqDesc*)(d + o_seq);
   dp.tiles = (const evisel::TextTile*)(d + o_tt);
   dp.frame_seq = (const int32_t*)(d + o_fs);
+  dp.blk_local = (const int32_t*)(d + o_bl);
   dp.n_items = (int32_t)P.items.size();
   dp.n_tiles = (int32_t)P.tiles.size();
   dp.n_seq = (int32_t)P.seqs.size();
@@ -111,11 +127,17 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   dp.hq = P.hq;
   dp.hkv = P.hkv;
   dp.Nv = P.layout.Nv;
+  dp.nb = (int32_t)P.blocks.size();
+  dp.W = P.hist_words;
+  int32_t hmax = 0;
+  for (int32_t loc : P.blk_local) hmax = std::max(hmax, loc);
+  dp.hmax = hmax;
+  dp.topp = P.rule.tau > 0.f ? 1 : 0;
   return EVISEL_OK;
 }
 
 struct WsLayout {
-  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, total;
+  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, total;
 };
 
 WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
@@ -134,22 +156,87 @@ WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
   w.seg = take((size_t)P.hq * P.segtot * 4);
   w.lse2t = take((size_t)P.hq * P.n_text_rows * 4);
   w.tmpart = take((size_t)P.hq * P.tiles.size() * 4);
+  if (P.rule.tau > 0.f) {
+    const size_t nb = P.blocks.size();
+    // bf16 keeps hi and lo (2 x 2 bytes), fp32 one float: 4 bytes either way
+    w.kbar = take((size_t)P.hkv * nb * d * 4);
+    w.rbits = take((size_t)P.hq * nb * P.hist_words * 64 * 4);
+    w.ubits = take((size_t)P.hq * nb * P.hist_words * 4);
+  } else {
+    w.kbar = w.rbits = w.ubits = 0;
+  }
   w.total = off;
   return w;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
+evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp) {
+  char* wb = (char*)workspace;
+  evisel::Workspace w;
+  w.pO = (float*)(wb + wl.pO);
+  w.pM = (float*)(wb + wl.pM);
+  w.pL = (float*)(wb + wl.pL);
+  w.pNV = (float*)(wb + wl.pNV);
+  w.seg = (float*)(wb + wl.seg);
+  w.lse2t = (float*)(wb + wl.lse2t);
+  w.tmpart = (float*)(wb + wl.tmpart);
+  w.kbar = topp ? (void*)(wb + wl.kbar) : nullptr;
+  w.rbits = topp ? (uint32_t*)(wb + wl.rbits) : nullptr;
+  w.ubits = topp ? (uint32_t*)(wb + wl.ubits) : nullptr;
+  return w;
+}
+
+// Checks shared by the compute calls that read q and k.
+evisel_status check_qk(const evisel::Plan& P, const void* q, const void* k,
+                       int32_t d, evisel_dtype dtype, float softmax_scale,
+                       void* workspace, size_t workspace_bytes,
+                       const WsLayout& wl) {
+  if (!q || !k) return fail(EVISEL_ERR_INVALID_ARG, "null q or k");
+  if (!aligned16(q) || !aligned16(k))
+    return fail(EVISEL_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
+    return fail(EVISEL_ERR_INVALID_ARG, "softmax_scale must be positive");
+  if (d != 64 && d != 128)
+    return fail(EVISEL_ERR_UNSUPPORTED, "head dim must be 64 or 128");
+  if (dtype != EVISEL_BF16 && dtype != EVISEL_FP32)
+    return fail(EVISEL_ERR_UNSUPPORTED, "dtype must be bf16 or fp32");
+  if (P.rule.block != 64)
+    return fail(EVISEL_ERR_UNSUPPORTED, "attention kernel needs block = 64");
+  if (!workspace || workspace_bytes < wl.total)
+    return fail(EVISEL_ERR_WORKSPACE,
+                "workspace needs " + std::to_string(wl.total) + " bytes");
+  if ((uintptr_t)workspace & 255)
+    return fail(EVISEL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return EVISEL_OK;
+}
+
+evisel::SelCall sel_call(const void* q, const void* k, int32_t d,
+                         evisel_dtype dtype, float softmax_scale, float tau,
+                         uint32_t* rbits, uint32_t* ubits) {
+  evisel::SelCall c;
+  c.q = q;
+  c.k = k;
+  c.scale_log2 = softmax_scale * 1.4426950408889634f;
+  c.tau = tau;
+  c.d = d;
+  c.fp32 = dtype == EVISEL_FP32;
+  c.rbits = rbits;
+  c.ubits = ubits;
+  return c;
+}
+
 // Kernel timing session (evisel_profile_begin / _end).
 struct Profile {
   bool open = false;
-  std::vector<hipEvent_t> ev;  // 4 per timed call
+  std::vector<hipEvent_t> ev;  // kProfEvents per timed call
   size_t used = 0;             // calls recorded
 };
 Profile g_prof;
+constexpr int kProfEvents = 5;
 
 void prof_record(size_t call, int k, hipStream_t s) {
-  (void)hipEventRecord(g_prof.ev[4 * call + k], s);
+  (void)hipEventRecord(g_prof.ev[kProfEvents * call + k], s);
 }
 
 evisel_status check_device(const evisel_mask* m) {
@@ -218,6 +305,8 @@ evisel_status evisel_mask_info(const evisel_mask* m, evisel_mask_stats* out) {
   out->hkv = P.hkv;
   out->block = P.rule.block;
   out->tokens_per_frame = P.layout.Nv;
+  out->hist_words = P.hist_words;
+  out->tau_p = P.rule.tau;
   return EVISEL_OK;
 }
 
@@ -278,38 +367,20 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
   const evisel::Plan& P = m->plan;
   if (n_layers < 1 || layer < 0 || layer >= n_layers)
     return fail(EVISEL_ERR_INVALID_ARG, "need 0 <= layer < n_layers");
-  if (!q || !k || !v || !out || !evidence)
-    return fail(EVISEL_ERR_INVALID_ARG, "null q, k, v, out or evidence");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
-    return fail(EVISEL_ERR_INVALID_ARG, "q, k, v, out must be 16-byte aligned");
-  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
-    return fail(EVISEL_ERR_INVALID_ARG, "softmax_scale must be positive");
-  if (d != 64 && d != 128)
-    return fail(EVISEL_ERR_UNSUPPORTED, "head dim must be 64 or 128");
-  if (dtype != EVISEL_BF16 && dtype != EVISEL_FP32)
-    return fail(EVISEL_ERR_UNSUPPORTED, "dtype must be bf16 or fp32");
-  if (P.rule.block != 64)
-    return fail(EVISEL_ERR_UNSUPPORTED, "attention kernel needs block = 64");
+  if (!v || !out || !evidence)
+    return fail(EVISEL_ERR_INVALID_ARG, "null v, out or evidence");
+  if (!aligned16(v) || !aligned16(out))
+    return fail(EVISEL_ERR_INVALID_ARG, "v and out must be 16-byte aligned");
+  const WsLayout wl = ws_layout(P, d);
+  st = check_qk(P, q, k, d, dtype, softmax_scale, workspace, workspace_bytes,
+                wl);
+  if (st != EVISEL_OK) return st;
   const int nv = P.layout.Nv;
   if (nv < 8 || 64 % nv != 0)
     return fail(EVISEL_ERR_UNSUPPORTED,
                 "tokens_per_frame must divide 64 and be >= 8");
-  const WsLayout wl = ws_layout(P, d);
-  if (!workspace || workspace_bytes < wl.total)
-    return fail(EVISEL_ERR_WORKSPACE,
-                "workspace needs " + std::to_string(wl.total) + " bytes");
-  if ((uintptr_t)workspace & 255)
-    return fail(EVISEL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-
-  char* wb = (char*)workspace;
-  evisel::Workspace w;
-  w.pO = (float*)(wb + wl.pO);
-  w.pM = (float*)(wb + wl.pM);
-  w.pL = (float*)(wb + wl.pL);
-  w.pNV = (float*)(wb + wl.pNV);
-  w.seg = (float*)(wb + wl.seg);
-  w.lse2t = (float*)(wb + wl.lse2t);
-  w.tmpart = (float*)(wb + wl.tmpart);
+  const bool topp = P.rule.tau > 0.f;
+  const evisel::Workspace w = carve(wl, workspace, topp);
   evisel::AttnCall c;
   c.q = q;
   c.k = k;
@@ -320,24 +391,66 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
   c.d = d;
   c.fp32 = dtype == EVISEL_FP32;
   hipStream_t s = (hipStream_t)stream;
-  const bool prof = g_prof.open && g_prof.used < g_prof.ev.size() / 4;
+  const bool prof =
+      g_prof.open && g_prof.used < g_prof.ev.size() / kProfEvents;
   const size_t call = g_prof.used;
   if (prof) prof_record(call, 0, s);
-  hipError_t e = evisel::launch_attention(m->dp, w, c, s);
-  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  hipError_t e = hipSuccess;
+  if (topp) {
+    e = evisel::launch_select(
+        m->dp, w,
+        sel_call(q, k, d, dtype, softmax_scale, P.rule.tau, w.rbits, w.ubits),
+        s);
+    if (e != hipSuccess) return hip_fail(e, "retention launch");
+    e = evisel::launch_seg_fill(m->dp, w, s);
+    if (e != hipSuccess) return hip_fail(e, "partial-mass fill launch");
+  }
   if (prof) prof_record(call, 1, s);
+  e = evisel::launch_attention(m->dp, w, c, s);
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  if (prof) prof_record(call, 2, s);
   e = evisel::launch_combine(m->dp, w, c, s);
   if (e != hipSuccess) return hip_fail(e, "combine launch");
-  if (prof) prof_record(call, 2, s);
+  if (prof) prof_record(call, 3, s);
   e = evisel::launch_evidence(
       m->dp, w, evidence + (size_t)layer * P.hq * P.T,
       text_mass ? text_mass + (size_t)layer * P.hq * P.seqs.size() : nullptr,
       s);
   if (e != hipSuccess) return hip_fail(e, "evidence launch");
   if (prof) {
-    prof_record(call, 3, s);
+    prof_record(call, 4, s);
     g_prof.used++;
   }
+  return EVISEL_OK;
+}
+
+evisel_status evisel_select_blocks(const evisel_mask* m, const void* q,
+                                   const void* k, int32_t d,
+                                   evisel_dtype dtype, float softmax_scale,
+                                   uint32_t* row_bits, uint32_t* block_bits,
+                                   void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  const evisel::Plan& P = m->plan;
+  if (!(P.rule.tau > 0.f))
+    return fail(EVISEL_ERR_INVALID_ARG,
+                "mask was built without top-p retention (tau_p = 0)");
+  if (!row_bits || !block_bits)
+    return fail(EVISEL_ERR_INVALID_ARG, "null row_bits or block_bits");
+  if (((uintptr_t)row_bits & 3) || ((uintptr_t)block_bits & 3))
+    return fail(EVISEL_ERR_INVALID_ARG, "bit arrays must be 4-byte aligned");
+  const WsLayout wl = ws_layout(P, d);
+  st = check_qk(P, q, k, d, dtype, softmax_scale, workspace, workspace_bytes,
+                wl);
+  if (st != EVISEL_OK) return st;
+  const evisel::Workspace w = carve(wl, workspace, true);
+  hipError_t e = evisel::launch_select(
+      m->dp, w,
+      sel_call(q, k, d, dtype, softmax_scale, P.rule.tau, row_bits,
+               block_bits),
+      (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "retention launch");
   return EVISEL_OK;
 }
 
@@ -370,7 +483,7 @@ evisel_status evisel_profile_begin(int32_t capacity) {
     return fail(EVISEL_ERR_INVALID_ARG, "a profiling session is open");
   g_prof = Profile();
   try {
-    g_prof.ev.resize((size_t)capacity * 4);
+    g_prof.ev.resize((size_t)capacity * kProfEvents);
   } catch (const std::bad_alloc&) {
     return fail(EVISEL_ERR_NOMEM, "host allocation failed");
   }
@@ -386,28 +499,27 @@ evisel_status evisel_profile_begin(int32_t capacity) {
   return EVISEL_OK;
 }
 
-evisel_status evisel_profile_end(double* ms_attention, double* ms_combine,
-                                 double* ms_evidence, int64_t* n_calls) {
+evisel_status evisel_profile_end(double* ms, int64_t* n_calls) {
   if (!g_prof.open)
     return fail(EVISEL_ERR_INVALID_ARG, "no profiling session is open");
-  double ms[3] = {0, 0, 0};
+  constexpr int kSpans = kProfEvents - 1;
+  double acc[kSpans] = {};
   hipError_t err = hipSuccess;
   for (size_t c = 0; c < g_prof.used && err == hipSuccess; ++c) {
-    err = hipEventSynchronize(g_prof.ev[4 * c + 3]);
-    for (int k = 0; k < 3 && err == hipSuccess; ++k) {
+    const hipEvent_t* ev = &g_prof.ev[kProfEvents * c];
+    err = hipEventSynchronize(ev[kSpans]);
+    for (int k = 0; k < kSpans && err == hipSuccess; ++k) {
       float t = 0.f;
-      err = hipEventElapsedTime(&t, g_prof.ev[4 * c + k],
-                                g_prof.ev[4 * c + k + 1]);
-      ms[k] += t;
+      err = hipEventElapsedTime(&t, ev[k], ev[k + 1]);
+      acc[k] += t;
     }
   }
   const int64_t used = (int64_t)g_prof.used;
   for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
   g_prof = Profile();
   if (err != hipSuccess) return hip_fail(err, "profile events");
-  if (ms_attention) *ms_attention = ms[0];
-  if (ms_combine) *ms_combine = ms[1];
-  if (ms_evidence) *ms_evidence = ms[2];
+  if (ms)
+    for (int k = 0; k < kSpans; ++k) ms[k] = acc[k];
   if (n_calls) *n_calls = used;
   return EVISEL_OK;
 }

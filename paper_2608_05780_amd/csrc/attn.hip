@@ -300,7 +300,7 @@ struct F32Path {
 };
 
 // ---------------------------------------------------------------------------
-template <class P, int D>
+template <class P, int D, bool TOPP>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
@@ -309,6 +309,9 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   constexpr int VSWZ = sizeof(T) == 2 ? kSwzV : kSwzNone;
   __shared__ __attribute__((aligned(1024))) char smem[4 * TB];
   EV_LDS char* lds = (EV_LDS char*)smem;   // [K0 | V0 | K1 | V1]
+  // top-p: CSR positions of the item's key tiles that some row retained
+  __shared__ short clist[TOPP ? kMaxItemCandidates : 1];
+  __shared__ int n_kept;
 
   const WorkItem it = pl.items[blockIdx.x];
   if (it.qblock < 0) return;
@@ -324,7 +327,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const int qrow = 32 * (wave & 1) + l32;
   const bool qvalid = active && qrow < qb.len;
   const int qpos = qb.start + qrow;
-  const int n = it.kb_end - it.kb_begin;
+  int n = it.kb_end - it.kb_begin;
   const float c2 = ac.scale_log2;
   const T* kg = (const T*)ac.k;
   const T* vg = (const T*)ac.v;
@@ -348,12 +351,58 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   auto vbuf = [&](int t) { return vbuf0 + (t & 1) * TB; };
   const int b0 = it.kb_begin;
 
+  // Top-p: a candidate tile is kept when it is always visible (system
+  // prefix, the query block itself) or some row of the item's heads
+  // retained it; wave 0 compacts the kept CSR positions into clist.
+  if constexpr (TOPP) {
+    if (wave == 0) {
+      const uint32_t* ub =
+          ws.ubits + ((size_t)it.head * pl.nb + it.qblock) * pl.W;
+      const size_t hstride = (size_t)pl.nb * pl.W;
+      int base = 0;
+      for (int c0 = 0; c0 < n; c0 += 64) {
+        const int t = c0 + lane;
+        bool keep = false;
+        if (t < n) {
+          const int bid = pl.col[b0 + t];
+          const int loc = pl.blk_local[bid];
+          if (loc < 0 || bid == it.qblock) {
+            keep = true;
+          } else {
+            unsigned wd = 0u;
+            for (int i = 0; i < it.nheads; ++i)
+              wd |= ub[i * hstride + (loc >> 5)];
+            keep = (wd >> (loc & 31)) & 1u;
+          }
+        }
+        const unsigned long long m = __ballot(keep);
+        const int pos = __builtin_amdgcn_mbcnt_hi(
+            (unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        if (keep) clist[base + pos] = (short)t;
+        base += __popcll(m);
+      }
+      if (lane == 0) n_kept = base;
+    }
+    __syncthreads();
+    n = __builtin_amdgcn_readfirstlane(n_kept);
+  }
+
   // Per tile, in three parts:
   //   pre:  causal / length mask (only on tiles that need it), row max and
   //         the (rare) lazy rescale of the accumulators;
   //   main: p = exp2(s * scale - m_ref) in place, row-sum partial;
   //   post: evidence partials of query-token rows, then O^T += V^T P^T.
-  auto tile_pre = [&](f32x16 (&s)[2], const BlockDesc& cur) {
+  auto tile_pre = [&](f32x16 (&s)[2], const BlockDesc& cur, unsigned rbit,
+                      int rloc) {
+    if (TOPP && rloc >= 0) {   // history block: rows that did not retain it
+      const bool kept = (rbit >> (rloc & 31)) & 1u;
+      if (__any(!kept)) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[c][r] = kept ? s[c][r] : neg_inf();
+      }
+    }
     if (cur.len < kTile || cur.start + cur.len - 1 > qb.start) {
 #pragma unroll
       for (int c = 0; c < 2; ++c)
@@ -436,15 +485,23 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   // BlockDesc of tile 64*batch + t, and the loop reads tile j's with
   // v_readlane. (Loading them per tile would put two dependent global round
   // trips in front of every tile's K/V loads.)
-  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0;
+  // Top-p: dsc_loc is the tile's local history index, or -1 when the tile
+  // is always visible.
+  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1;
   auto load_batch = [&](int batch) {
     const int t = batch * 64 + lane;
     if (t < n) {
-      const BlockDesc bd = pl.blocks[pl.col[b0 + t]];
+      const int pos = TOPP ? (int)clist[t] : t;
+      const int bid = pl.col[b0 + pos];
+      const BlockDesc bd = pl.blocks[bid];
       dsc_start = bd.start;
       dsc_len = bd.len;
       dsc_region = bd.region;
       dsc_aux = bd.aux;
+      if (TOPP) {
+        const int loc = pl.blk_local[bid];
+        dsc_loc = bid == it.qblock ? -1 : loc;
+      }
     }
   };
   auto desc = [&](int t) {
@@ -457,25 +514,48 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     return d;
   };
 
+  // Top-p: the row's retained-history word of a tile, fetched with the
+  // tile's key/value loads.
+  const uint32_t* rrow =
+      TOPP ? ws.rbits + ((size_t)h * pl.nb + it.qblock) * pl.W * 64 + qrow
+           : nullptr;
+  auto row_bits = [&](int loc) -> unsigned {
+    return loc < 0 ? ~0u : rrow[(size_t)(loc >> 5) * 64];
+  };
+  auto loc_of = [&](int t) {
+    return TOPP ? __builtin_amdgcn_readlane(dsc_loc, t & 63) : -1;
+  };
+
   // Tile j+1 streams into the other buffer pair while tile j is computed.
   load_batch(0);
   BlockDesc kb = desc(0);
-  kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
-  vload.issue(vbuf(0), vg, kb.start, kb.len, kvh, wave);
+  int lnext = loc_of(0);
+  unsigned wnext = 0u;
+  if (n > 0) {
+    kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
+    vload.issue(vbuf(0), vg, kb.start, kb.len, kvh, wave);
+    if (TOPP) wnext = row_bits(lnext);
+  }
   for (int j = 0; j < n; ++j) {
     const BlockDesc cur = kb;
+    const int lcur = lnext;
     if (((j + 1) & 63) == 0 && j + 1 < n) load_batch((j + 1) >> 6);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const unsigned wcur = wnext;
     __syncthreads();
     if (j + 1 < n) {
       kb = desc(j + 1);
       kload.issue(kbuf(j + 1), kg, kb.start, kb.len, kvh, wave);
       vload.issue(vbuf(j + 1), vg, kb.start, kb.len, kvh, wave);
+      if (TOPP) {
+        lnext = loc_of(j + 1);
+        wnext = row_bits(lnext);
+      }
     }
     if (active) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
       P::qk(s, kbuf(j), qf, l32, g);
-      tile_pre(s, cur);
+      tile_pre(s, cur, wcur, lcur);
       const float ts = tile_main(s);
       tile_post(s, cur, ts, vbuf(j));
     }
@@ -596,16 +676,31 @@ hipError_t launch_attention(const DevPlan& p, const Workspace& w,
                             const AttnCall& c, hipStream_t s) {
   if (p.n_items == 0) return hipSuccess;
   dim3 grid(p.n_items), block(kThreads);
+  if (p.topp) {
+    if (c.fp32) {
+      if (c.d == 64)
+        attn_kernel<F32Path<64>, 64, true><<<grid, block, 0, s>>>(p, w, c);
+      else
+        attn_kernel<F32Path<128>, 128, true><<<grid, block, 0, s>>>(p, w, c);
+    } else {
+      if (c.d == 64)
+        attn_kernel<Bf16Path<64>, 64, true><<<grid, block, 0, s>>>(p, w, c);
+      else
+        attn_kernel<Bf16Path<128>, 128, true><<<grid, block, 0, s>>>(p, w,
+                                                                     c);
+    }
+    return hipGetLastError();
+  }
   if (c.fp32) {
     if (c.d == 64)
-      attn_kernel<F32Path<64>, 64><<<grid, block, 0, s>>>(p, w, c);
+      attn_kernel<F32Path<64>, 64, false><<<grid, block, 0, s>>>(p, w, c);
     else
-      attn_kernel<F32Path<128>, 128><<<grid, block, 0, s>>>(p, w, c);
+      attn_kernel<F32Path<128>, 128, false><<<grid, block, 0, s>>>(p, w, c);
   } else {
     if (c.d == 64)
-      attn_kernel<Bf16Path<64>, 64><<<grid, block, 0, s>>>(p, w, c);
+      attn_kernel<Bf16Path<64>, 64, false><<<grid, block, 0, s>>>(p, w, c);
     else
-      attn_kernel<Bf16Path<128>, 128><<<grid, block, 0, s>>>(p, w, c);
+      attn_kernel<Bf16Path<128>, 128, false><<<grid, block, 0, s>>>(p, w, c);
   }
   return hipGetLastError();
 }

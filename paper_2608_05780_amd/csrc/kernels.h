@@ -14,10 +14,15 @@ struct DevPlan {
   const SeqDesc* seqs;
   const TextTile* tiles;
   const int32_t* frame_seq;
+  const int32_t* blk_local;  // [nb] local selectable index, -1 for system
   int32_t n_items, n_tiles, n_seq;
   int32_t S, T, n_text_rows;
   int64_t segtot;
   int32_t hq, hkv, Nv;
+  int32_t nb;                // blocks
+  int32_t W;                 // history words per row (top-p)
+  int32_t hmax;              // longest block history (top-p)
+  int32_t topp;              // 1: adaptive top-p retention
 };
 
 // Workspace carve-up for one prefill call.
@@ -29,6 +34,21 @@ struct Workspace {
   float* seg;    // [hq][segtot]    log2 partial mass per (query row, frame)
   float* lse2t;  // [hq][n_text_rows] log2 LSE of query rows
   float* tmpart; // [hq][n_tiles]   non-visual mass per query tile
+  // top-p retention (null for the static rule)
+  void* kbar;              // bf16: hi [hkv][nb][d] then lo; fp32: [hkv][nb][d]
+  uint32_t* rbits;         // [hq][nb][W][64] retained history per row
+  uint32_t* ubits;         // [hq][nb][W]     union over the block's rows
+};
+
+struct SelCall {
+  const void* q;
+  const void* k;
+  float scale_log2;        // softmax scale * log2(e)
+  float tau;
+  int32_t d;
+  int32_t fp32;
+  uint32_t* rbits;         // outputs (workspace or caller buffers)
+  uint32_t* ubits;
 };
 
 struct AttnCall {
@@ -44,6 +64,16 @@ struct AttnCall {
 
 hipError_t launch_attention(const DevPlan& p, const Workspace& w,
                             const AttnCall& c, hipStream_t s);
+// Top-p retention: mean keys, then per (block, head) the retained history
+// of every row (rbits) and the union over the block's rows (ubits).
+// LDS bytes the retention kernel needs at its narrowest setting.
+size_t select_lds_need(int nh_max, int W);
+hipError_t launch_select(const DevPlan& p, const Workspace& w,
+                         const SelCall& c, hipStream_t s);
+// Sets the per-(row, frame) partial masses to -inf (top-p: key tiles no row
+// of a work item retained are skipped and leave no partial).
+hipError_t launch_seg_fill(const DevPlan& p, const Workspace& w,
+                           hipStream_t s);
 hipError_t launch_combine(const DevPlan& p, const Workspace& w,
                           const AttnCall& c, hipStream_t s);
 hipError_t launch_evidence(const DevPlan& p, const Workspace& w,

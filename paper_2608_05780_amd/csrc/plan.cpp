@@ -33,6 +33,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   if (R.block < 1) return "block must be >= 1";
   if (R.sink < 0) return "sink_blocks must be >= 0";
   if (R.window < -1) return "window must be >= 0 or -1";
+  if (!(R.tau >= 0.f && R.tau <= 1.f)) return "tau_p must be in [0, 1]";
   if (hq < 1 || hkv < 1 || hq % hkv != 0)
     return "head counts must satisfy hq >= 1, hkv >= 1, hq % hkv == 0";
   if (hq > 4096) return "hq too large";
@@ -42,6 +43,9 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   P.layout = L;
   if (P.layout.n_sys.empty()) P.layout.n_sys.assign(nseq, 0);
   P.rule = R;
+  const bool topp = R.tau > 0.f;
+  // top-p: every causal block is a candidate
+  const int32_t window = topp ? -1 : R.window;
   P.hq = hq;
   P.hkv = hkv;
 
@@ -109,7 +113,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     const int32_t nvb = (int32_t)vb.size();
     for (int32_t i = 0; i < nvb; ++i) {        // visual rows
       rowlist.assign(sb.begin(), sb.end());
-      const int32_t lo = R.window < 0 ? 0 : std::max(0, i - R.window);
+      const int32_t lo = window < 0 ? 0 : std::max(0, i - window);
       for (int32_t b = 0; b < std::min(R.sink, lo); ++b)
         rowlist.push_back(vb[b]);
       for (int32_t b = lo; b <= i; ++b) rowlist.push_back(vb[b]);
@@ -130,6 +134,18 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   for (int32_t b = 0; b < nb; ++b) P.row_ptr[b + 1] += P.row_ptr[b];
   if ((int64_t)P.row_ptr[nb] != (int64_t)P.col.size())
     return "internal error: CSR size mismatch";
+
+  // ---- selectable blocks (top-p bookkeeping) -------------------------------
+  P.blk_local.assign(nb, -1);
+  int32_t max_sel = 0;
+  for (size_t n = 0; n < nseq; ++n) {
+    int32_t j = 0;
+    for (int32_t b : visb[n]) P.blk_local[b] = j++;
+    for (int32_t b : txtb[n]) P.blk_local[b] = j++;
+    max_sel = std::max(max_sel, j);
+  }
+  // bits for history blocks 0 .. max_sel - 2
+  P.hist_words = std::max(1, (max_sel - 1 + 31) / 32);
 
   // ---- work items ---------------------------------------------------------
   const int32_t group = hq / hkv;
@@ -232,6 +248,9 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     }
   // drop trailing padding
   while (!P.items.empty() && P.items.back().qblock < 0) P.items.pop_back();
+  for (const WorkItem& w : P.items)
+    P.max_item_candidates =
+        std::max(P.max_item_candidates, w.kb_end - w.kb_begin);
   return "";
 }
 

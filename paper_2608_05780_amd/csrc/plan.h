@@ -65,9 +65,18 @@ struct Layout {
   int32_t Nv = 0;
 };
 
+// Sparse rule. tau > 0 selects the paper's adaptive top-p retention: the
+// candidate key blocks of a row are then its whole causal history (the CSR
+// is the all-causal one) and the retained subset is decided per (head, row)
+// on the device; sink and window are ignored.
 struct Rule {
   int32_t block = 64, sink = 1, window = -1;
+  float tau = 0.f;
 };
+
+// Top-p mode: most candidate key blocks one attention work item may hold
+// (its compacted list lives in LDS).
+constexpr int kMaxItemCandidates = 2048;
 
 struct Plan {
   // inputs
@@ -84,6 +93,13 @@ struct Plan {
   std::vector<SeqDesc> seqs;
   std::vector<TextTile> tiles;
   std::vector<int32_t> frame_seq;   // [T] video of each global frame
+  // top-p retention: per block its index among its video's selectable
+  // (non-system) blocks in token order (-1 for system blocks); a block's
+  // history H is local blocks [0, local). hist_words 32-bit words hold one
+  // row's retained-history bits.
+  std::vector<int32_t> blk_local;
+  int32_t hist_words = 0;
+  int32_t max_item_candidates = 0;
 };
 
 // Builds the plan; returns "" on success or an error message.

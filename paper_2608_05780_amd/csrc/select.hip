@@ -1,0 +1,446 @@
+// Adaptive top-p block retention for gfx950 (appendix "Detailed Sparse
+// Prefilling": mean-key block representative, block affinity over the
+// history H_i, softmax over H_i, smallest subset whose probability reaches
+// tau_p).
+//
+// pool_kernel    kbar_j = mean of block j's keys per kv head, an fp32 sum in
+//                token order divided by the block length. For bf16 inputs
+//                kbar is kept as two bf16 values, hi = RNE(kbar) and
+//                lo = RNE(kbar - hi), so the affinity can run on bf16 MFMA
+//                while kbar keeps about 16 significant bits.
+// select_kernel  one work-group per (query block, query head). The block's
+//                rows share their history (local blocks 0 .. nh-1 of the
+//                video). Affinities g = q . kbar * scale * log2(e) come from
+//                32x32x16 bf16 MFMA, hi and lo accumulated into one fp32
+//                tile (fp32 inputs: 32x32x2 f32 MFMA), and are staged in LDS,
+//                each row owned by TPR consecutive lanes (TPR/4 quads). Per
+//                row: e_j = exp2(g_j - max), Z = sum e_j, threshold
+//                tau * Z. The retained set is {j : e_j >= t*} for the
+//                largest t* whose tail mass F(t*) = sum_{e_j >= t*} e_j still
+//                reaches the threshold. t* is found by bisection over the
+//                bit patterns of the non-negative fp32 e_j (ordered like the
+//                values), stopping once a single candidate value is left.
+//                When several e_j equal t*, they are retained in ascending
+//                block order until the threshold is reached. Every sum runs
+//                in a fixed order, F is monotone in t, and the lanes of a row
+//                see identical reductions, so the result is bitwise
+//                reproducible.
+// seg_fill_kernel  -inf into the per-(row, frame) partial masses before a
+//                top-p attention pass (tiles that no row of a work item
+//                retained are skipped and write nothing).
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace evisel {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kSelThreads = 256;
+constexpr size_t kSelLdsTwoPerCu = 80 * 1024;
+constexpr size_t kSelLdsMax = 160 * 1024;
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
+
+template <bool F32, int D>
+__global__ __launch_bounds__(D) void pool_kernel(const DevPlan pl,
+                                                 const void* __restrict__ k,
+                                                 void* __restrict__ kbar) {
+  const int b = blockIdx.x, kvh = blockIdx.y, c = threadIdx.x;
+  const BlockDesc bd = pl.blocks[b];
+  if (bd.region == kSys) return;
+  const size_t rs = (size_t)pl.hkv * D;
+  const size_t base = ((size_t)bd.start * pl.hkv + kvh) * D + c;
+  float s = 0.f;
+  if (F32) {
+    const float* src = (const float*)k + base;
+    for (int r = 0; r < bd.len; ++r) s += src[r * rs];
+  } else {
+    const __bf16* src = (const __bf16*)k + base;
+    for (int r = 0; r < bd.len; ++r) s += (float)src[r * rs];
+  }
+  const float m = s / (float)bd.len;
+  const size_t o = ((size_t)kvh * pl.nb + b) * D + c;
+  if (F32) {
+    ((float*)kbar)[o] = m;
+  } else {
+    const __bf16 hi = (__bf16)m;
+    const __bf16 lo = (__bf16)(m - (float)hi);
+    ((__bf16*)kbar)[o] = hi;
+    ((__bf16*)kbar)[(size_t)pl.hkv * pl.nb * D + o] = lo;
+  }
+}
+
+// Reductions over the TPR lanes of a row (TPR = 4, 8 or 16 consecutive
+// lanes). Each step combines a lane with a partner that holds the same
+// partial as the lane's own mirror image, so every lane of the group ends
+// with the same bits (fp addition is commutative).
+template <int CTRL>
+__device__ __forceinline__ int dpp(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, dpp<CTRL>(__builtin_bit_cast(int, x)));
+}
+constexpr int kQuadSwap1 = 0xB1;      // quad_perm [1, 0, 3, 2]
+constexpr int kQuadSwap2 = 0x4E;      // quad_perm [2, 3, 0, 1]
+constexpr int kHalfMirror = 0x141;    // lane i <-> 7 - i within 8
+constexpr int kRowMirror = 0x140;     // lane i <-> 15 - i within 16
+
+template <int TPR>
+__device__ __forceinline__ float grp_sum(float x) {
+  x += dppf<kQuadSwap1>(x);
+  x += dppf<kQuadSwap2>(x);
+  if (TPR >= 8) x += dppf<kHalfMirror>(x);
+  if (TPR >= 16) x += dppf<kRowMirror>(x);
+  return x;
+}
+template <int TPR>
+__device__ __forceinline__ int grp_sumi(int x) {
+  x += dpp<kQuadSwap1>(x);
+  x += dpp<kQuadSwap2>(x);
+  if (TPR >= 8) x += dpp<kHalfMirror>(x);
+  if (TPR >= 16) x += dpp<kRowMirror>(x);
+  return x;
+}
+template <int TPR>
+__device__ __forceinline__ float grp_max(float x) {
+  x = fmaxf(x, dppf<kQuadSwap1>(x));
+  x = fmaxf(x, dppf<kQuadSwap2>(x));
+  if (TPR >= 8) x = fmaxf(x, dppf<kHalfMirror>(x));
+  if (TPR >= 16) x = fmaxf(x, dppf<kRowMirror>(x));
+  return x;
+}
+template <int TPR>
+__device__ __forceinline__ unsigned grp_minu(unsigned x) {
+  x = min(x, (unsigned)dpp<kQuadSwap1>((int)x));
+  x = min(x, (unsigned)dpp<kQuadSwap2>((int)x));
+  if (TPR >= 8) x = min(x, (unsigned)dpp<kHalfMirror>((int)x));
+  if (TPR >= 16) x = min(x, (unsigned)dpp<kRowMirror>((int)x));
+  return x;
+}
+template <int TPR>
+__device__ __forceinline__ unsigned grp_maxu(unsigned x) {
+  x = max(x, (unsigned)dpp<kQuadSwap1>((int)x));
+  x = max(x, (unsigned)dpp<kQuadSwap2>((int)x));
+  if (TPR >= 8) x = max(x, (unsigned)dpp<kHalfMirror>((int)x));
+  if (TPR >= 16) x = max(x, (unsigned)dpp<kRowMirror>((int)x));
+  return x;
+}
+
+// Values per thread and LDS row stride (in floats) for a history of nh
+// blocks; both multiples of 4 so rows can be read as 16-byte vectors.
+__host__ __device__ inline int sel_per_thread(int nh, int tpr) {
+  return ((nh + tpr - 1) / tpr + 3) & ~3;
+}
+__host__ __device__ inline int sel_stride(int nh, int tpr) {
+  return tpr * sel_per_thread(nh, tpr) + 4;
+}
+inline size_t sel_lds_bytes(int nh, int tpr, int W) {
+  return (size_t)(kSelThreads / tpr) * sel_stride(nh, tpr) * 4 +
+         (size_t)64 * W * 4;
+}
+
+template <bool F32, int D, int TPR>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    const DevPlan pl, const Workspace ws, const SelCall sc) {
+  constexpr int RPW = kSelThreads / TPR;          // rows per pass
+  constexpr int NRG = RPW >= 32 ? RPW / 32 : 1;   // 32-row MFMA groups
+  constexpr int WPG = 4 / NRG;                    // waves per row group
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  const int qbid = blockIdx.x, h = blockIdx.y;
+  const BlockDesc qb = pl.blocks[qbid];
+  const int nh = pl.blk_local[qbid];              // |H|; -1 for system rows
+  const int W = pl.W;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint32_t* const rb = sc.rbits + ((size_t)h * pl.nb + qbid) * W * 64;
+  uint32_t* const ub = sc.ubits + ((size_t)h * pl.nb + qbid) * W;
+  if (nh <= 0) {                                  // empty history
+    for (int i = tid; i < W * 64; i += kSelThreads) rb[i] = 0u;
+    for (int i = tid; i < W; i += kSelThreads) ub[i] = 0u;
+    return;
+  }
+  const int L = sel_per_thread(nh, TPR);
+  const int stride = sel_stride(nh, TPR);
+  float* const ev = dyn;                                  // [RPW][stride]
+  uint32_t* const wb = (uint32_t*)(dyn + RPW * stride);   // [64][W]
+  for (int i = tid; i < 64 * W; i += kSelThreads) wb[i] = 0u;
+
+  const int kvh = h / (pl.hq / pl.hkv);
+  const int first = qbid - nh;                    // global id of local 0
+  const int l32 = lane & 31, g = lane >> 5;
+  const int rg = wave % NRG, ph = wave / NRG;
+  const int ntile = (nh + 31) / 32;
+
+  for (int r0 = 0; r0 < qb.len; r0 += RPW) {
+    // ---- affinities of rows r0 .. r0 + RPW - 1 against the history ----
+    {
+      const int rl = rg * 32 + l32;
+      const bool rv = rl < RPW && r0 + rl < qb.len;
+      const size_t qoff = ((size_t)(qb.start + r0 + rl) * pl.hq + h) * D;
+      if (!F32) {
+        bf16x8 qf[D / 16];
+        const __bf16* qs = (const __bf16*)sc.q + qoff + 8 * g;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) {
+          bf16x8 z = {};
+          qf[kk] = rv ? *(const bf16x8*)(qs + 16 * kk) : z;
+        }
+        const __bf16* kh0 = (const __bf16*)ws.kbar +
+                            ((size_t)kvh * pl.nb + first) * D + 8 * g;
+        const size_t lo_off = (size_t)pl.hkv * pl.nb * D;
+        for (int t = ph; t < ntile; t += WPG) {
+          const int jb = min(32 * t + l32, nh - 1);
+          const __bf16* kh = kh0 + (size_t)jb * D;
+          f32x16 acc = {};
+#pragma unroll
+          for (int kk = 0; kk < D / 16; ++kk) {
+            const bf16x8 ah = *(const bf16x8*)(kh + 16 * kk);
+            const bf16x8 al = *(const bf16x8*)(kh + lo_off + 16 * kk);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, qf[kk], acc, 0,
+                                                          0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qf[kk], acc, 0,
+                                                          0, 0);
+          }
+          if (rv) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+              if (j < nh) ev[rl * stride + j] = acc[r] * sc.scale_log2;
+            }
+          }
+        }
+      } else {
+        float qf[D / 2];
+        const float* qs = (const float*)sc.q + qoff + g * (D / 2);
+#pragma unroll
+        for (int u = 0; u < D / 8; ++u) {
+          f32x4 z = {};
+          const f32x4 v = rv ? *(const f32x4*)(qs + 4 * u) : z;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) qf[4 * u + e] = v[e];
+        }
+        const float* k0 = (const float*)ws.kbar +
+                          ((size_t)kvh * pl.nb + first) * D + g * (D / 2);
+        for (int t = ph; t < ntile; t += WPG) {
+          const int jb = min(32 * t + l32, nh - 1);
+          const float* kr = k0 + (size_t)jb * D;
+          f32x16 acc = {};
+#pragma unroll
+          for (int u = 0; u < D / 8; ++u) {
+            const f32x4 a = *(const f32x4*)(kr + 4 * u);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], qf[4 * u + e],
+                                                         acc, 0, 0, 0);
+          }
+          if (rv) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+              if (j < nh) ev[rl * stride + j] = acc[r] * sc.scale_log2;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- retention of each row (TPR lanes per row) ----
+    {
+      const int rr = tid / TPR, part = tid % TPR;
+      const int row = r0 + rr;
+      if (row < qb.len) {                         // uniform over the group
+        const int j0 = part * L;
+        const int cnt = max(0, min(L, nh - j0));  // real entries
+        float* const my = ev + rr * stride + j0;
+        float mx = neg_inf();
+        for (int i = 0; i < cnt; ++i) mx = fmaxf(mx, my[i]);
+        mx = grp_max<TPR>(mx);
+        float z = 0.f;
+        unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
+        for (int i = 0; i < L; i += 4) {
+          f32x4 v = *(const f32x4*)(my + i);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = i + e < cnt;
+            const float x = ok ? __builtin_amdgcn_exp2f(v[e] - mx) : 0.f;
+            v[e] = x;
+            z += x;
+            if (ok) {
+              kmin = min(kmin, __float_as_uint(x));
+              kmax = max(kmax, __float_as_uint(x));
+            }
+          }
+          *(f32x4*)(my + i) = v;
+        }
+        z = grp_sum<TPR>(z);
+        kmin = grp_minu<TPR>(kmin);
+        kmax = grp_maxu<TPR>(kmax);
+        const float thr = sc.tau * z;
+        // F(lo) >= thr > F(hi); clo / chi count the entries >= lo / >= hi
+        unsigned lo = kmin, hi = kmax + 1u;
+        int clo = nh, chi = 0;
+        float fhi = 0.f;
+        while (hi - lo > 1u && clo - chi > 1) {
+          const unsigned mid = lo + ((hi - lo) >> 1);
+          float f = 0.f;
+          int c = 0;
+          for (int i = 0; i < L; i += 4) {
+            const f32x4 v = *(const f32x4*)(my + i);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bool in = __float_as_uint(v[e]) >= mid;
+              f += in ? v[e] : 0.f;
+              c += in;
+            }
+          }
+          f = grp_sum<TPR>(f);
+          c = grp_sumi<TPR>(c);
+          if (f >= thr) {
+            lo = mid;
+            clo = c;
+          } else {
+            hi = mid;
+            chi = c;
+            fhi = f;
+          }
+        }
+        // Several entries equal to lo: keep them in block order while the
+        // retained mass is still below the threshold.
+        const bool tie = clo - chi > 1;
+        int take = 0, before = 0;
+        if (tie) {
+          const float et = __uint_as_float(lo);
+          float cum = fhi;
+          const int nt = clo - chi;
+          while (take < nt && cum < thr) {
+            cum += et;
+            ++take;
+          }
+          int mine = 0;
+          for (int i = 0; i < cnt; ++i) mine += __float_as_uint(my[i]) == lo;
+          for (int q2 = 0; q2 < TPR; ++q2) {
+            const int o = __shfl(mine, lane - part + q2);
+            before += q2 < part ? o : 0;
+          }
+        }
+        unsigned word = 0u;
+        int wcur = j0 >> 5, rank = before;
+        uint32_t* const wrow = wb + row * W;
+        for (int i = 0; i < cnt; ++i) {
+          const int j = j0 + i;
+          const unsigned kb = __float_as_uint(my[i]);
+          bool sel = kb >= lo;
+          if (tie && kb == lo) sel = rank++ < take;
+          if ((j >> 5) != wcur) {
+            if (word) atomicOr(wrow + wcur, word);
+            word = 0u;
+            wcur = j >> 5;
+          }
+          word |= (unsigned)sel << (j & 31);
+        }
+        if (word) atomicOr(wrow + wcur, word);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- per-row bits [W][64] and the union over the block's rows ----
+  for (int i = tid; i < 64 * W; i += kSelThreads) {
+    const int w = i >> 6, r = i & 63;
+    rb[i] = wb[r * W + w];
+  }
+  for (int w = tid; w < W; w += kSelThreads) {
+    unsigned u = 0u;
+    for (int r = 0; r < 64; ++r) u |= wb[r * W + w];
+    ub[w] = u;
+  }
+}
+
+__global__ void seg_fill_kernel(float* __restrict__ p, size_t n) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += stride)
+    p[i] = neg_inf();
+}
+
+template <bool F32, int D, int TPR>
+hipError_t launch_sel(const DevPlan& p, const Workspace& w, const SelCall& c,
+                      size_t lds, hipStream_t s) {
+  auto* fn = select_kernel<F32, D, TPR>;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(
+        (const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+        (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  fn<<<dim3(p.nb, p.hq), dim3(kSelThreads), lds, s>>>(p, w, c);
+  return hipGetLastError();
+}
+
+template <bool F32, int D>
+hipError_t launch_sel_d(const DevPlan& p, const Workspace& w,
+                        const SelCall& c, int nh_max, hipStream_t s) {
+  // widest rows per pass whose LDS still lets two work-groups share a CU
+  const int tprs[3] = {4, 8, 16};
+  int pick = -1;
+  for (int i = 0; i < 3 && pick < 0; ++i)
+    if (sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsTwoPerCu) pick = i;
+  for (int i = 0; i < 3 && pick < 0; ++i)
+    if (sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsMax) pick = i;
+  if (pick < 0) return hipErrorInvalidValue;
+  const size_t lds = sel_lds_bytes(nh_max, tprs[pick], p.W);
+  if (pick == 0) return launch_sel<F32, D, 4>(p, w, c, lds, s);
+  if (pick == 1) return launch_sel<F32, D, 8>(p, w, c, lds, s);
+  return launch_sel<F32, D, 16>(p, w, c, lds, s);
+}
+
+}  // namespace
+
+size_t select_lds_need(int nh_max, int W) {
+  return sel_lds_bytes(nh_max, 16, W);
+}
+
+hipError_t launch_select(const DevPlan& p, const Workspace& w,
+                         const SelCall& c, hipStream_t s) {
+  if (c.fp32) {
+    if (c.d == 64)
+      pool_kernel<true, 64><<<dim3(p.nb, p.hkv), dim3(64), 0, s>>>(p, c.k,
+                                                                   w.kbar);
+    else
+      pool_kernel<true, 128><<<dim3(p.nb, p.hkv), dim3(128), 0, s>>>(p, c.k,
+                                                                     w.kbar);
+  } else {
+    if (c.d == 64)
+      pool_kernel<false, 64><<<dim3(p.nb, p.hkv), dim3(64), 0, s>>>(p, c.k,
+                                                                    w.kbar);
+    else
+      pool_kernel<false, 128><<<dim3(p.nb, p.hkv), dim3(128), 0, s>>>(
+          p, c.k, w.kbar);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nh_max = std::max(p.hmax, 1);
+  if (c.fp32)
+    return c.d == 64 ? launch_sel_d<true, 64>(p, w, c, nh_max, s)
+                     : launch_sel_d<true, 128>(p, w, c, nh_max, s);
+  return c.d == 64 ? launch_sel_d<false, 64>(p, w, c, nh_max, s)
+                   : launch_sel_d<false, 128>(p, w, c, nh_max, s);
+}
+
+hipError_t launch_seg_fill(const DevPlan& p, const Workspace& w,
+                           hipStream_t s) {
+  const size_t n = (size_t)p.hq * p.segtot;
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  seg_fill_kernel<<<dim3(blocks), dim3(256), 0, s>>>(w.seg, n);
+  return hipGetLastError();
+}
+
+}  // namespace evisel

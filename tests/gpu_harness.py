@@ -46,7 +46,7 @@ def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
     ns, nf, nt = wl.layout_arrays(w, seed)
     mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
                                w.sink_blocks, w.window, w.hq, w.hkv,
-                               n_sys=ns)
+                               n_sys=ns, tau_p=w.tau_p)
     st = mask.stats
     S, T, nseq = st["n_tokens"], st["n_frames_total"], len(nf)
     L = len(layers)

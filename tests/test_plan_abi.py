@@ -33,10 +33,10 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(raw, name), name
 
 
-def _plan(n_frames, n_text, Nv, rule, hq=4, hkv=2, n_sys=None):
+def _plan(n_frames, n_text, Nv, rule, hq=4, hkv=2, n_sys=None, tau_p=0.0):
     return ev.build_block_mask(n_frames, n_text, Nv, rule.block,
                                rule.sink_blocks, rule.window, hq, hkv,
-                               n_sys=n_sys, host_only=True)
+                               n_sys=n_sys, host_only=True, tau_p=tau_p)
 
 
 CASES = [
@@ -117,6 +117,26 @@ def _check_work(m, csr, hq):
     assert sorted(slots) == list(range(m.stats["n_chunk_slots"]))
 
 
+@pytest.mark.parametrize("ci", range(len(CASES)))
+def test_topp_plan_is_all_causal_candidates(lib, ci):
+    """Top-p masks take every causal block as a candidate (the retained
+    subset is decided on the device): the CSR equals the all-causal rule's,
+    and the history word count covers the longest selectable history."""
+    ns, nf, nt, Nv, rule = CASES[ci]
+    m = _plan(nf, nt, Nv, rule, n_sys=ns, tau_p=0.97)
+    causal = Rule(rule.block, 0, -1)
+    lay = Layout(ns, nf, nt, Nv)
+    blk, rp, col = oblocks.active_csr(lay, causal, brute=lay.S < 3000)
+    got = ev.mask_export(m)
+    np.testing.assert_array_equal(got["row_ptr"], rp)
+    np.testing.assert_array_equal(got["col"], col)
+    from oracle import topp
+    b = topp.Blocks(lay, rule.block)
+    assert m.stats["hist_words"] == max(1, -(-(b.max_count - 1) // 32))
+    assert abs(m.stats["tau_p"] - 0.97) < 1e-7
+    _check_work(m, got, 4)
+
+
 def _status(fn):
     with pytest.raises(ev.EviselError) as ei:
         fn()
@@ -138,6 +158,13 @@ def test_error_codes(lib):
         ev.ERR_INVALID_ARG
     assert _status(lambda: _plan([3], [2], 64, r, n_sys=[-1])) == \
         ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, r, tau_p=1.5)) == \
+        ev.ERR_INVALID_ARG
+    assert _status(lambda: _plan([3], [2], 64, r, tau_p=-0.25)) == \
+        ev.ERR_INVALID_ARG
+    # more candidate key blocks per query block than the kernel's list holds
+    assert _status(lambda: _plan([2100], [2], 64, r, tau_p=0.9)) == \
+        ev.ERR_UNSUPPORTED
     # compute calls refuse a host-only plan before touching the device
     m = _plan([3], [2], 64, r)
     st = lib.evisel_sparse_prefill(m.handle, 0, 1, None, None, None, 128, 0,
@@ -150,4 +177,7 @@ def test_error_codes(lib):
     assert lib.evisel_sparse_prefill_workspace(m.handle, 96) == 0
     assert lib.evisel_sparse_prefill_workspace(m.handle, 128) > 0
     assert lib.evisel_mask_info(None, None) == ev.ERR_INVALID_ARG
+    st = lib.evisel_select_blocks(m.handle, None, None, 128, 0, 0.1, None,
+                                  None, None, 0, None)
+    assert st == ev.ERR_INVALID_ARG
     lib.evisel_mask_free(None)                   # ignored

@@ -21,6 +21,14 @@ Draw protocol (fixed, so the oracle and the GPU see bit-identical inputs):
   which does not change any value.
 * Q ``[S, Hq, d]``, K and V ``[S, Hkv, d]`` are i.i.d. N(0, 1) float32; u is a
   unit vector in R^d (float32).
+* Optional frame structure (``key_struct = (beta, gamma, rho)``, off in the
+  paper-shaped configs): per video and kv head an AR(1) sequence of frame
+  content vectors c_0 = xi_0, c_f = rho c_{f-1} + sqrt(1 - rho^2) xi_f
+  (xi ~ N(0, I_d), drawn from stream 3 * CHUNKS + 1, videos in order, then
+  frames, kv heads, dimensions); the K rows of frame f get ``+ beta c_f``
+  and the visual Q rows of frame f (every q head of the kv head) get
+  ``+ gamma c_f``. It gives the keys the block-level content and the queries
+  the locality that make a block-affinity selection sparse.
 * Planting: every kv head's K rows of a planted frame f get ``+ s_f * u`` and
   every q head's query-token rows get ``+ s_Q * u`` (float32 arithmetic).
 * bf16 workloads are then rounded to bf16 with round-to-nearest-even; the
@@ -63,6 +71,8 @@ class Workload:
     n_videos: int = 1
     ragged_frames: tuple = ()       # (lo, hi) inclusive, ragged batch only
     plant_args: dict = field(default_factory=dict)
+    tau_p: float = 0.0              # > 0: adaptive top-p retention rule
+    key_struct: tuple = ()          # (beta, gamma, rho) frame structure
 
     @property
     def softmax_scale(self) -> float:
@@ -270,7 +280,7 @@ def gen_layer(w: Workload, layer: int, seed: int = 0,
     ns, nf, nt = layout_arrays(w, seed)
     tok0, vis0, txt0, end = token_ranges(w, seed)
     S = int(end[-1])
-    kids = _streams(w, seed)[layer + 1].spawn(3 * CHUNKS + 1)
+    kids = _streams(w, seed)[layer + 1].spawn(3 * CHUNKS + 2)
     q = np.empty((S, w.hq, w.d), np.float32)
     k = np.empty((S, w.hkv, w.d), np.float32)
     v = np.empty((S, w.hkv, w.d), np.float32)
@@ -290,8 +300,25 @@ def gen_layer(w: Workload, layer: int, seed: int = 0,
     rng = np.random.Generator(np.random.PCG64(kids[3 * CHUNKS]))
     u = rng.standard_normal(w.d, dtype=np.float32).astype(np.float64)
     u = (u / np.linalg.norm(u)).astype(np.float32)
-    strength, _, s_q = plant_table(w, seed)
     Nv = w.tokens_per_frame
+    if w.key_struct:
+        beta, gamma, rho = (float(x) for x in w.key_struct)
+        srng = np.random.Generator(np.random.PCG64(kids[3 * CHUNKS + 1]))
+        grp = w.hq // w.hkv
+        for n in range(len(nf)):
+            F = int(nf[n])
+            xi = srng.standard_normal((F, w.hkv, w.d), dtype=np.float32)
+            c = np.empty_like(xi)
+            c[0] = xi[0]
+            a_r = np.float32(rho)
+            b_r = np.float32(np.sqrt(1.0 - rho * rho))
+            for f in range(1, F):
+                c[f] = a_r * c[f - 1] + b_r * xi[f]
+            toks = c.repeat(Nv, axis=0)                  # [F * Nv, hkv, d]
+            a, e = int(vis0[n]), int(vis0[n]) + F * Nv
+            k[a:e] += np.float32(beta) * toks
+            q[a:e] += np.float32(gamma) * np.repeat(toks, grp, axis=1)
+    strength, _, s_q = plant_table(w, seed)
     foff = 0
     for n in range(len(nf)):
         F = int(nf[n])
