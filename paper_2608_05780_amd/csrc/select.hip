@@ -145,6 +145,214 @@ inline size_t sel_lds_bytes(int nh, int tpr, int W) {
          (size_t)64 * W * 4;
 }
 
+// Retention of one row whose TPR lanes hold e-candidates g_j (log2 units) in
+// LDS, entries [j0, j0 + cnt) of the row's history at my[0 .. cnt). Sets the
+// retained history bits in wrow (LDS, OR). Both variants compute the same
+// result; retain_row_regs keeps the lane's L <= kRegVals values in registers.
+constexpr int kRegVals = 36;
+
+// Bits [j0, j0 + n) of a row from a lane's mask (n <= 64, j0 % 4 == 0).
+__device__ __forceinline__ void or_bits(uint32_t* wrow, int j0,
+                                        unsigned long long m) {
+  if (!m) return;
+  const int w0 = j0 >> 5, off = j0 & 31;
+  const unsigned long long lo = m << off;
+  const unsigned long long hi = off ? m >> (64 - off) : 0ull;
+  if ((unsigned)lo) atomicOr(wrow + w0, (unsigned)lo);
+  if ((unsigned)(lo >> 32)) atomicOr(wrow + w0 + 1, (unsigned)(lo >> 32));
+  if ((unsigned)hi) atomicOr(wrow + w0 + 2, (unsigned)hi);
+}
+
+template <int TPR>
+__device__ __forceinline__ void retain_row_regs(const float* my, int L,
+                                                int cnt, int nh, int j0,
+                                                float tau, int lane, int part,
+                                                uint32_t* wrow) {
+  constexpr int NCK = kRegVals / 4;
+  const int nck = L >> 2;                         // uniform per work-group
+  // Entries past the history read as -inf, so their e is +0; the cut t*
+  // found below is never 0 (F at any key up to the smallest positive e is
+  // the whole sum Z >= tau Z), so zeros are never retained or counted as
+  // ties, and no validity mask is needed after the load.
+  float v[kRegVals];
+#pragma unroll
+  for (int c = 0; c < NCK; ++c) {
+    f32x4 t = {};
+    if (c < nck) t = *(const f32x4*)(my + 4 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[4 * c + e] = 4 * c + e < cnt ? t[e] : neg_inf();
+  }
+  float mx = neg_inf();
+#pragma unroll
+  for (int i = 0; i < kRegVals; ++i) mx = fmaxf(mx, v[i]);
+  mx = grp_max<TPR>(mx);
+  float z = 0.f;
+  unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+  for (int i = 0; i < kRegVals; ++i) {
+    const float x = __builtin_amdgcn_exp2f(v[i] - mx);
+    v[i] = x;
+    z += x;
+    const unsigned kb = __float_as_uint(x);
+    kmin = min(kmin, kb ? kb : 0xFFFFFFFFu);
+    kmax = max(kmax, kb);
+  }
+  z = grp_sum<TPR>(z);
+  kmin = grp_minu<TPR>(kmin);
+  kmax = grp_maxu<TPR>(kmax);
+  const float thr = tau * z;
+  // F(lo) >= thr > F(hi); clo / chi count the entries >= lo / >= hi
+  unsigned lo = kmin, hi = kmax + 1u;
+  int clo = nh, chi = 0;
+  float fhi = 0.f;
+  while (hi - lo > 1u && clo - chi > 1) {
+    const unsigned mid = lo + ((hi - lo) >> 1);
+    float f = 0.f;
+    int k = 0;
+#pragma unroll
+    for (int c = 0; c < NCK; ++c) {
+      if (c < nck) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool in = __float_as_uint(v[4 * c + e]) >= mid;
+          f += in ? v[4 * c + e] : 0.f;
+          k += in;
+        }
+      }
+    }
+    f = grp_sum<TPR>(f);
+    k = grp_sumi<TPR>(k);
+    if (f >= thr) {
+      lo = mid;
+      clo = k;
+    } else {
+      hi = mid;
+      chi = k;
+      fhi = f;
+    }
+  }
+  const bool tie = clo - chi > 1;
+  int take = 0, rank = 0;
+  if (tie) {
+    const float et = __uint_as_float(lo);
+    float cum = fhi;
+    const int nt = clo - chi;
+    while (take < nt && cum < thr) {
+      cum += et;
+      ++take;
+    }
+    int mine = 0;
+#pragma unroll
+    for (int i = 0; i < kRegVals; ++i) mine += __float_as_uint(v[i]) == lo;
+    for (int q2 = 0; q2 < TPR; ++q2) {
+      const int o = __shfl(mine, lane - part + q2);
+      rank += q2 < part ? o : 0;
+    }
+  }
+  unsigned long long m = 0ull;
+#pragma unroll
+  for (int i = 0; i < kRegVals; ++i) {
+    const unsigned kb = __float_as_uint(v[i]);
+    bool sel = kb >= lo;
+    if (tie && kb == lo) sel = rank++ < take;
+    m |= (unsigned long long)sel << i;
+  }
+  or_bits(wrow, j0, m);
+}
+
+template <int TPR>
+__device__ __forceinline__ void retain_row_lds(float* my, int L, int cnt,
+                                               int nh, int j0, float tau,
+                                               int lane, int part,
+                                               uint32_t* wrow) {
+  float mx = neg_inf();
+  for (int i = 0; i < L; i += 4) {
+    const f32x4 t = *(const f32x4*)(my + i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (i + e < cnt) mx = fmaxf(mx, t[e]);
+  }
+  mx = grp_max<TPR>(mx);
+  float z = 0.f;
+  unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int i = 0; i < L; i += 4) {
+    f32x4 t = *(const f32x4*)(my + i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = i + e < cnt;
+      const float x = ok ? __builtin_amdgcn_exp2f(t[e] - mx) : 0.f;
+      t[e] = x;
+      z += x;
+      if (ok) {
+        kmin = min(kmin, __float_as_uint(x));
+        kmax = max(kmax, __float_as_uint(x));
+      }
+    }
+    *(f32x4*)(my + i) = t;
+  }
+  z = grp_sum<TPR>(z);
+  kmin = grp_minu<TPR>(kmin);
+  kmax = grp_maxu<TPR>(kmax);
+  const float thr = tau * z;
+  unsigned lo = kmin, hi = kmax + 1u;
+  int clo = nh, chi = 0;
+  float fhi = 0.f;
+  while (hi - lo > 1u && clo - chi > 1) {
+    const unsigned mid = lo + ((hi - lo) >> 1);
+    float f = 0.f;
+    int k = 0;
+#pragma unroll 2
+    for (int i = 0; i < L; i += 4) {
+      const f32x4 t = *(const f32x4*)(my + i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool in = __float_as_uint(t[e]) >= mid;
+        f += in ? t[e] : 0.f;
+        k += in;
+      }
+    }
+    f = grp_sum<TPR>(f);
+    k = grp_sumi<TPR>(k);
+    if (f >= thr) {
+      lo = mid;
+      clo = k;
+    } else {
+      hi = mid;
+      chi = k;
+      fhi = f;
+    }
+  }
+  const bool tie = clo - chi > 1;
+  int take = 0, rank = 0;
+  if (tie) {
+    const float et = __uint_as_float(lo);
+    float cum = fhi;
+    const int nt = clo - chi;
+    while (take < nt && cum < thr) {
+      cum += et;
+      ++take;
+    }
+    int mine = 0;
+    for (int i = 0; i < cnt; ++i) mine += __float_as_uint(my[i]) == lo;
+    for (int q2 = 0; q2 < TPR; ++q2) {
+      const int o = __shfl(mine, lane - part + q2);
+      rank += q2 < part ? o : 0;
+    }
+  }
+  // 32 entries at a time (j0 % 4 == 0, so a run covers at most 2 words)
+  for (int i0 = 0; i0 < cnt; i0 += 32) {
+    unsigned long long m = 0ull;
+    for (int i = i0; i < min(cnt, i0 + 32); ++i) {
+      const unsigned kb = __float_as_uint(my[i]);
+      bool sel = kb >= lo;
+      if (tie && kb == lo) sel = rank++ < take;
+      m |= (unsigned long long)sel << (i - i0);
+    }
+    or_bits(wrow, j0 + i0, m);
+  }
+}
+
 template <bool F32, int D, int TPR>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const DevPlan pl, const Workspace ws, const SelCall sc) {
@@ -259,93 +467,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         const int j0 = part * L;
         const int cnt = max(0, min(L, nh - j0));  // real entries
         float* const my = ev + rr * stride + j0;
-        float mx = neg_inf();
-        for (int i = 0; i < cnt; ++i) mx = fmaxf(mx, my[i]);
-        mx = grp_max<TPR>(mx);
-        float z = 0.f;
-        unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
-        for (int i = 0; i < L; i += 4) {
-          f32x4 v = *(const f32x4*)(my + i);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool ok = i + e < cnt;
-            const float x = ok ? __builtin_amdgcn_exp2f(v[e] - mx) : 0.f;
-            v[e] = x;
-            z += x;
-            if (ok) {
-              kmin = min(kmin, __float_as_uint(x));
-              kmax = max(kmax, __float_as_uint(x));
-            }
-          }
-          *(f32x4*)(my + i) = v;
-        }
-        z = grp_sum<TPR>(z);
-        kmin = grp_minu<TPR>(kmin);
-        kmax = grp_maxu<TPR>(kmax);
-        const float thr = sc.tau * z;
-        // F(lo) >= thr > F(hi); clo / chi count the entries >= lo / >= hi
-        unsigned lo = kmin, hi = kmax + 1u;
-        int clo = nh, chi = 0;
-        float fhi = 0.f;
-        while (hi - lo > 1u && clo - chi > 1) {
-          const unsigned mid = lo + ((hi - lo) >> 1);
-          float f = 0.f;
-          int c = 0;
-          for (int i = 0; i < L; i += 4) {
-            const f32x4 v = *(const f32x4*)(my + i);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bool in = __float_as_uint(v[e]) >= mid;
-              f += in ? v[e] : 0.f;
-              c += in;
-            }
-          }
-          f = grp_sum<TPR>(f);
-          c = grp_sumi<TPR>(c);
-          if (f >= thr) {
-            lo = mid;
-            clo = c;
-          } else {
-            hi = mid;
-            chi = c;
-            fhi = f;
-          }
-        }
-        // Several entries equal to lo: keep them in block order while the
-        // retained mass is still below the threshold.
-        const bool tie = clo - chi > 1;
-        int take = 0, before = 0;
-        if (tie) {
-          const float et = __uint_as_float(lo);
-          float cum = fhi;
-          const int nt = clo - chi;
-          while (take < nt && cum < thr) {
-            cum += et;
-            ++take;
-          }
-          int mine = 0;
-          for (int i = 0; i < cnt; ++i) mine += __float_as_uint(my[i]) == lo;
-          for (int q2 = 0; q2 < TPR; ++q2) {
-            const int o = __shfl(mine, lane - part + q2);
-            before += q2 < part ? o : 0;
-          }
-        }
-        unsigned word = 0u;
-        int wcur = j0 >> 5, rank = before;
         uint32_t* const wrow = wb + row * W;
-        for (int i = 0; i < cnt; ++i) {
-          const int j = j0 + i;
-          const unsigned kb = __float_as_uint(my[i]);
-          bool sel = kb >= lo;
-          if (tie && kb == lo) sel = rank++ < take;
-          if ((j >> 5) != wcur) {
-            if (word) atomicOr(wrow + wcur, word);
-            word = 0u;
-            wcur = j >> 5;
-          }
-          word |= (unsigned)sel << (j & 31);
-        }
-        if (word) atomicOr(wrow + wcur, word);
+        if (L <= kRegVals)
+          retain_row_regs<TPR>(my, L, cnt, nh, j0, sc.tau, lane, part, wrow);
+        else
+          retain_row_lds<TPR>(my, L, cnt, nh, j0, sc.tau, lane, part, wrow);
       }
     }
     __syncthreads();
@@ -387,9 +513,15 @@ hipError_t launch_sel(const DevPlan& p, const Workspace& w, const SelCall& c,
 template <bool F32, int D>
 hipError_t launch_sel_d(const DevPlan& p, const Workspace& w,
                         const SelCall& c, int nh_max, hipStream_t s) {
-  // widest rows per pass whose LDS still lets two work-groups share a CU
+  // fewest lanes per row whose share of the longest history fits in
+  // registers (and whose LDS lets two work-groups share a CU); else the
+  // LDS-streaming variant with the widest rows that fit
   const int tprs[3] = {4, 8, 16};
   int pick = -1;
+  for (int i = 0; i < 3 && pick < 0; ++i)
+    if (sel_per_thread(nh_max, tprs[i]) <= kRegVals &&
+        sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsTwoPerCu)
+      pick = i;
   for (int i = 0; i < 3 && pick < 0; ++i)
     if (sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsTwoPerCu) pick = i;
   for (int i = 0; i < 3 && pick < 0; ++i)

@@ -293,6 +293,16 @@ def test_topp_skips_tiles_and_is_deterministic():
     np.testing.assert_array_equal(res.E, res2.E)
 
 
+def test_topp_long_history_streams_from_lds():
+    # 600 visual blocks: a row's share of its history no longer fits the
+    # register variant, so the retention streams it from LDS
+    w = _small("long-history", d=64, hq=2, hkv=1, tokens_per_frame=64,
+               n_frames=(600,), n_text=(40,), n_sys=(6,), tau_p=TAU,
+               key_struct=(1.0, 1.0, 0.9))
+    say("case long history")
+    _run_case(w, rows_budget=256)
+
+
 def test_topp_config2_layer():
     w = wl.get(2, tau_p=TAU)
     say("case config-2 top-p")
