@@ -26,11 +26,13 @@ What it computes (each function cites the passage it follows):
                    softmax, smallest subset reaching tau_p) and the attention
                    and evidence it induces (appendix, "Detailed Sparse
                    Prefilling").
+* ``cues``      -- the cross-frame cue A_ff and its timestamp-aligned E_ff,
+                   and the intra-frame cue A_if (Evidence Decomposition).
 
 Parity pins live in ``tests/`` (brute force, closed forms, a library attention
 routine, invariants, planted ranking). No function here is "parity unpinned".
 """
-from . import layout, attention, aggregate, blocks, brute, topp  # noqa: F401
+from . import layout, attention, aggregate, blocks, brute, topp, cues  # noqa: F401
 from .layout import Layout, Rule  # noqa: F401
 from .attention import run_layer, attend  # noqa: F401
 from .aggregate import frame_evidence, topk_per_video  # noqa: F401

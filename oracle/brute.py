@@ -78,3 +78,25 @@ def attention(q, k, v, n_sys, n_frames, n_text, Nv, B, sink, window, scale):
                     else:
                         tm[h][toks[i][0]] += ex[j] / z
     return O, LSE, E, tm
+
+
+def probabilities(q, k, n_sys, n_frames, n_text, Nv, B, sink, window, scale):
+    """Per (head, query token) the softmax probabilities over its visible
+    keys, as {key token: probability} dicts: P[h][i]. Also returns the token
+    table of ``_tokens`` (video, region, position in region, global frame)."""
+    toks = _tokens(n_sys, n_frames, n_text, Nv)
+    S = len(toks)
+    hq, hkv, d = len(q[0]), len(k[0]), len(q[0][0])
+    P = [[None] * S for _ in range(hq)]
+    for h in range(hq):
+        g = h // (hq // hkv)
+        for i in range(S):
+            keys = [m for m in range(S)
+                    if _visible(toks[i], toks[m], i, m, B, sink, window)]
+            logits = [math.fsum(q[i][h][c] * k[m][g][c] for c in range(d)) *
+                      scale for m in keys]
+            mx = max(logits)
+            ex = [math.exp(x - mx) for x in logits]
+            z = math.fsum(ex)
+            P[h][i] = {m: ex[j] / z for j, m in enumerate(keys)}
+    return P, toks
