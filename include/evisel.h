@@ -101,6 +101,8 @@ typedef struct {
   int32_t hq, hkv, block, tokens_per_frame;
   int32_t hist_words;      /* W: 32-bit words of one row's history bits   */
   float tau_p;             /* the rule's tau_p                            */
+  int64_t n_frame_pairs;   /* (frame, earlier frame) pairs the pattern can
+                              connect: entries of the cross-frame cue      */
 } evisel_mask_stats;
 
 /* Builds the block partition, the compact list of active block pairs (CSR,
@@ -151,6 +153,17 @@ evisel_status evisel_mask_export_work(const evisel_mask* mask, int32_t* qblock,
  * evisel_select_blocks) needs for head dim d. */
 size_t evisel_sparse_prefill_workspace(const evisel_mask* mask, int32_t d);
 
+/* Extra workspace bytes, on top of evisel_sparse_prefill_workspace, that an
+ * evisel_sparse_prefill call with frame_pairs or intra_frame needs. */
+size_t evisel_cue_workspace(const evisel_mask* mask, int32_t d);
+
+/* Copies the frame pairs of the cross-frame cue (n_frame_pairs entries) into
+ * host buffers: query frame a and earlier key frame b (global frame ids, same
+ * video). Pair i is entry i of evisel_sparse_prefill's frame_pairs. Either
+ * pointer may be NULL. */
+evisel_status evisel_mask_export_pairs(const evisel_mask* mask, int32_t* a,
+                                       int32_t* b);
+
 /* Top-p retention of one layer alone (appendix, mean-key, affinity and
  * probability equations and the smallest subset reaching tau_p; see
  * evisel_mask_rule). evisel_sparse_prefill runs the same kernels itself;
@@ -196,7 +209,19 @@ evisel_status evisel_select_blocks(const evisel_mask* mask, const void* q,
  *   text_mass device [n_layers, Hq, n_seq] fp32 or NULL; slice [layer] gets
  *            the same rows' mass on non-visual keys (system prefix and query
  *            tokens); per video sum_f E + text_mass = n_text
- *   workspace device, >= evisel_sparse_prefill_workspace(mask, d) bytes
+ *   frame_pairs device [n_layers, n_frame_pairs] fp32 or NULL: the
+ *            cross-frame cue (Evidence Decomposition, A_ff). Entry i of
+ *            slice [layer] is, for pair (a, b) of evisel_mask_export_pairs,
+ *            the mean over heads and over frame a's N_v rows of the row's
+ *            total probability on frame b's visual tokens. Pairs outside
+ *            the list are 0.
+ *   intra_frame device [n_layers, T, N_v, N_v] fp32 or NULL: the intra-frame
+ *            cue (A_if; flattened per timestamp it is E_if). Slice [layer]
+ *            [t][i][m] is the head mean of the probability of frame t's
+ *            token i on its token m (0 for m > i).
+ *   workspace device, >= evisel_sparse_prefill_workspace(mask, d) bytes,
+ *            plus evisel_cue_workspace(mask, d) when frame_pairs or
+ *            intra_frame is given
  * Requires B = 64, N_v dividing 64 with N_v >= 8 (when any video has
  * query rows reducing onto frames), 0 <= layer < n_layers.
  * Errors: INVALID_ARG (NULL buffer, host-only mask, layer out of range),
@@ -206,7 +231,8 @@ evisel_status evisel_sparse_prefill(const evisel_mask* mask, int32_t layer,
                                     const void* k, const void* v, int32_t d,
                                     evisel_dtype dtype, float softmax_scale,
                                     void* out, float* lse, float* evidence,
-                                    float* text_mass, void* workspace,
+                                    float* text_mass, float* frame_pairs,
+                                    float* intra_frame, void* workspace,
                                     size_t workspace_bytes, void* stream);
 
 /* Aggregates evidence [n_layers, Hq, T] (Evidence Decomposition: mean over
@@ -219,23 +245,33 @@ evisel_status evisel_sparse_prefill(const evisel_mask* mask, int32_t layer,
  *   topk_idx   device [sum of clamped k] int32: per video, in video order,
  *              the k local frame indices with the largest e_qf, ordered by
  *              (e_qf descending, index ascending); NaN ranks as -inf
+ *   frame_pairs device [n_layers, n_frame_pairs] from evisel_sparse_prefill,
+ *              or NULL
+ *   e_ff       device [n_layers, T] or NULL (needs frame_pairs): the
+ *              timestamp-aligned cross-frame evidence. For frame t at local
+ *              index t' of a video with F frames: the mean over its t'
+ *              earlier frames b of A_ff[t, b] and the mean over its F-1-t'
+ *              later frames a of A_ff[a, t], averaged over the sides that
+ *              exist (0 for a one-frame video)
  * Errors: INVALID_ARG, UNSUPPORTED (a video with more than 65536 frames
  * when top-k is requested), HIP. */
 evisel_status evisel_frame_evidence(const evisel_mask* mask,
                                     const float* evidence, int32_t n_layers,
                                     float* e_qf_layer, float* e_qf,
                                     const int32_t* k_per_seq,
-                                    int32_t* topk_idx, void* stream);
+                                    int32_t* topk_idx,
+                                    const float* frame_pairs, float* e_ff,
+                                    void* stream);
 
-/* Kernel timing, a tracing aid. evisel_profile_begin creates 5 * capacity
+/* Kernel timing, a tracing aid. evisel_profile_begin creates 6 * capacity
  * HIP events on the current device; each later evisel_sparse_prefill call,
  * up to `capacity` calls, records events on its stream before the top-p
  * retention (empty for a static mask), before the attention kernel, after
- * it, after the split-row combine and after the evidence reduction.
- * evisel_profile_end waits for those events, writes the summed milliseconds
- * of the four spans into ms[0..3] (retention, attention, combine, evidence)
- * and the number of timed calls (either pointer may be NULL) and destroys
- * the events. One session at a time per process; not thread-safe. Errors:
+ * it, after the split-row combine, after the evidence reduction and after
+ * the frame cues (empty when none is requested). evisel_profile_end waits
+ * for those events, writes the summed milliseconds of the five spans into
+ * ms[0..4] (retention, attention, combine, evidence, cues) and the number
+ * of timed calls (either pointer may be NULL) and destroys the events. One session at a time per process; not thread-safe. Errors:
  * INVALID_ARG (capacity < 1, a session already open or none open), NOMEM,
  * HIP. */
 evisel_status evisel_profile_begin(int32_t capacity);

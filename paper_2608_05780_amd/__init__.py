@@ -20,7 +20,7 @@ from typing import Optional, Sequence
 
 __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "sparse_prefill_workspace", "sparse_prefill", "frame_evidence",
-           "select_blocks", "unpack_row_bits",
+           "select_blocks", "unpack_row_bits", "mask_export_pairs",
            "mask_info", "mask_export", "mask_export_work", "profile_begin",
            "profile_end", "LIB_PATH"]
 
@@ -50,7 +50,7 @@ class _Stats(ctypes.Structure):
         "n_active_pairs", "n_work_items", "n_text_tiles", "n_chunk_slots")] + \
         [(n, ctypes.c_int32) for n in ("hq", "hkv", "block",
                                        "tokens_per_frame", "hist_words")] + \
-        [("tau_p", ctypes.c_float)]
+        [("tau_p", ctypes.c_float), ("n_frame_pairs", ctypes.c_int64)]
 
 
 _lib = None
@@ -75,14 +75,20 @@ _SIGS = {
         ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_size_t, ctypes.c_void_p]),
+    "evisel_cue_workspace": (ctypes.c_size_t, [ctypes.c_void_p,
+                                               ctypes.c_int32]),
+    "evisel_mask_export_pairs": (ctypes.c_int, [ctypes.c_void_p, _i32p,
+                                                _i32p]),
     "evisel_select_blocks": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
         ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "evisel_frame_evidence": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
-        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p]),
     "evisel_profile_begin": (ctypes.c_int, [ctypes.c_int32]),
     "evisel_profile_end": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]),
@@ -219,8 +225,24 @@ def mask_export_work(mask: Mask) -> dict:
     return {k: v[:n] for k, v in out.items()}
 
 
-def sparse_prefill_workspace(mask: Mask, d: int) -> int:
-    return int(load().evisel_sparse_prefill_workspace(mask.handle, d))
+def sparse_prefill_workspace(mask: Mask, d: int, cues: bool = False) -> int:
+    """Workspace bytes of a prefill call (``cues``: with frame-cue
+    outputs)."""
+    n = int(load().evisel_sparse_prefill_workspace(mask.handle, d))
+    if cues:
+        n += int(load().evisel_cue_workspace(mask.handle, d))
+    return n
+
+
+def mask_export_pairs(mask: Mask) -> dict:
+    """Frame pairs (a, b) of the cross-frame cue, in output order."""
+    import numpy as np
+    n = mask.stats["n_frame_pairs"]
+    a = np.zeros(max(n, 1), np.int32)
+    b = np.zeros(max(n, 1), np.int32)
+    p = lambda x: x.ctypes.data_as(_i32p)
+    _check(load().evisel_mask_export_pairs(mask.handle, p(a), p(b)))
+    return {"a": a[:n], "b": b[:n]}
 
 
 def _dtype_code(t) -> int:
@@ -234,17 +256,20 @@ def _dtype_code(t) -> int:
 
 def sparse_prefill(mask: Mask, layer: int, n_layers: int, q, k, v, out,
                    evidence, workspace, lse=None, text_mass=None,
-                   softmax_scale: Optional[float] = None, stream=None):
+                   softmax_scale: Optional[float] = None, stream=None,
+                   frame_pairs=None, intra_frame=None):
     """One probe layer. Tensors are contiguous torch tensors on the GPU:
     q/out [S, Hq, d], k/v [S, Hkv, d] (bf16 or fp32), evidence
     [n_layers, Hq, T] fp32, lse [Hq, S] fp32, text_mass [n_layers, Hq, n_seq]
-    fp32, workspace a uint8 tensor of sparse_prefill_workspace() bytes."""
+    fp32, frame_pairs [n_layers, n_frame_pairs] fp32, intra_frame
+    [n_layers, T, N_v, N_v] fp32, workspace a uint8 tensor of
+    sparse_prefill_workspace(mask, d, cues) bytes."""
     d = int(q.shape[-1])
     scale = float(softmax_scale) if softmax_scale is not None else d ** -0.5
     _check(load().evisel_sparse_prefill(
         mask.handle, layer, n_layers, _ptr(q), _ptr(k), _ptr(v), d,
         _dtype_code(q), scale, _ptr(out), _ptr(lse), _ptr(evidence),
-        _ptr(text_mass), _ptr(workspace),
+        _ptr(text_mass), _ptr(frame_pairs), _ptr(intra_frame), _ptr(workspace),
         0 if workspace is None else workspace.numel() * workspace.element_size(),
         _stream(stream)))
 
@@ -275,12 +300,15 @@ def unpack_row_bits(bits, n_hist: int):
 
 
 def frame_evidence(mask: Mask, evidence, n_layers: int, e_qf,
-                   e_qf_layer=None, k_per_seq=None, topk=None, stream=None):
+                   e_qf_layer=None, k_per_seq=None, topk=None, stream=None,
+                   frame_pairs=None, e_ff=None):
     """Head/layer aggregation and top-k. ``k_per_seq`` is a device int32
-    tensor [n_seq]; ``topk`` a device int32 tensor [sum k]."""
+    tensor [n_seq]; ``topk`` a device int32 tensor [sum k]; ``e_ff``
+    [n_layers, T] needs the prefill's ``frame_pairs``."""
     _check(load().evisel_frame_evidence(
         mask.handle, _ptr(evidence), n_layers, _ptr(e_qf_layer), _ptr(e_qf),
-        _ptr(k_per_seq), _ptr(topk), _stream(stream)))
+        _ptr(k_per_seq), _ptr(topk), _ptr(frame_pairs), _ptr(e_ff),
+        _stream(stream)))
 
 
 def profile_begin(capacity: int):
@@ -290,8 +318,8 @@ def profile_begin(capacity: int):
 
 def profile_end() -> dict:
     """Finish the timing session: summed ms per kernel and the call count."""
-    ms = (ctypes.c_double * 4)()
+    ms = (ctypes.c_double * 5)()
     n = ctypes.c_int64()
     _check(load().evisel_profile_end(ms, ctypes.byref(n)))
     return {"select_ms": ms[0], "attention_ms": ms[1], "combine_ms": ms[2],
-            "evidence_ms": ms[3], "calls": n.value}
+            "evidence_ms": ms[3], "cues_ms": ms[4], "calls": n.value}

@@ -96,7 +96,9 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   const size_t o_blk = put(buf, P.blocks), o_col = put(buf, P.col),
                o_it = put(buf, P.items), o_seq = put(buf, P.seqs),
                o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq),
-               o_bl = put(buf, P.blk_local);
+               o_bl = put(buf, P.blk_local), o_fp = put(buf, P.pairs),
+               o_fop = put(buf, P.ff_out_ptr), o_foi = put(buf, P.ff_out_idx),
+               o_fip = put(buf, P.ff_in_ptr), o_fii = put(buf, P.ff_in_idx);
   hipError_t e = hipGetDevice(&m->device);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   e = hipMalloc(&m->dev, buf.size());
@@ -117,6 +119,13 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   dp.tiles = (const evisel::TextTile*)(d + o_tt);
   dp.frame_seq = (const int32_t*)(d + o_fs);
   dp.blk_local = (const int32_t*)(d + o_bl);
+  dp.pairs = (const evisel::FramePair*)(d + o_fp);
+  dp.ff_out_ptr = (const int32_t*)(d + o_fop);
+  dp.ff_out_idx = (const int32_t*)(d + o_foi);
+  dp.ff_in_ptr = (const int32_t*)(d + o_fip);
+  dp.ff_in_idx = (const int32_t*)(d + o_fii);
+  dp.n_pairs = (int32_t)P.pairs.size();
+  dp.nnz = (int32_t)P.col.size();
   dp.n_items = (int32_t)P.items.size();
   dp.n_tiles = (int32_t)P.tiles.size();
   dp.n_seq = (int32_t)P.seqs.size();
@@ -138,6 +147,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
 
 struct WsLayout {
   size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, total;
+  size_t segv, lse2v, cue_total;   // frame cues, after `total`
 };
 
 WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
@@ -166,12 +176,18 @@ WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
     w.kbar = w.rbits = w.ubits = 0;
   }
   w.total = off;
+  const int fpt = P.layout.Nv >= 1 && 64 % P.layout.Nv == 0
+                      ? 64 / P.layout.Nv : 1;
+  w.segv = take((size_t)P.hq * P.col.size() * fpt * 64 * 4);
+  w.lse2v = take((size_t)P.hq * P.S * 4);
+  w.cue_total = off - w.total;
   return w;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp) {
+evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp,
+                        bool cues = false) {
   char* wb = (char*)workspace;
   evisel::Workspace w;
   w.pO = (float*)(wb + wl.pO);
@@ -184,6 +200,8 @@ evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp) {
   w.kbar = topp ? (void*)(wb + wl.kbar) : nullptr;
   w.rbits = topp ? (uint32_t*)(wb + wl.rbits) : nullptr;
   w.ubits = topp ? (uint32_t*)(wb + wl.ubits) : nullptr;
+  w.segv = cues ? (float*)(wb + wl.segv) : nullptr;
+  w.lse2v = cues ? (float*)(wb + wl.lse2v) : nullptr;
   return w;
 }
 
@@ -233,7 +251,7 @@ struct Profile {
   size_t used = 0;             // calls recorded
 };
 Profile g_prof;
-constexpr int kProfEvents = 5;
+constexpr int kProfEvents = 6;
 
 void prof_record(size_t call, int k, hipStream_t s) {
   (void)hipEventRecord(g_prof.ev[kProfEvents * call + k], s);
@@ -307,6 +325,7 @@ evisel_status evisel_mask_info(const evisel_mask* m, evisel_mask_stats* out) {
   out->tokens_per_frame = P.layout.Nv;
   out->hist_words = P.hist_words;
   out->tau_p = P.rule.tau;
+  out->n_frame_pairs = (int64_t)P.pairs.size();
   return EVISEL_OK;
 }
 
@@ -360,7 +379,8 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
                                     const void* k, const void* v, int32_t d,
                                     evisel_dtype dtype, float softmax_scale,
                                     void* out, float* lse, float* evidence,
-                                    float* text_mass, void* workspace,
+                                    float* text_mass, float* frame_pairs,
+                                    float* intra_frame, void* workspace,
                                     size_t workspace_bytes, void* stream) {
   evisel_status st = check_device(m);
   if (st != EVISEL_OK) return st;
@@ -380,7 +400,14 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
     return fail(EVISEL_ERR_UNSUPPORTED,
                 "tokens_per_frame must divide 64 and be >= 8");
   const bool topp = P.rule.tau > 0.f;
-  const evisel::Workspace w = carve(wl, workspace, topp);
+  const bool cues = frame_pairs || intra_frame;
+  if (cues && workspace_bytes < wl.total + wl.cue_total)
+    return fail(EVISEL_ERR_WORKSPACE,
+                "frame cues need " + std::to_string(wl.total + wl.cue_total) +
+                    " bytes of workspace");
+  if (cues && ((uintptr_t)frame_pairs & 3 || (uintptr_t)intra_frame & 3))
+    return fail(EVISEL_ERR_INVALID_ARG, "cue outputs must be 4-byte aligned");
+  const evisel::Workspace w = carve(wl, workspace, topp, cues);
   evisel::AttnCall c;
   c.q = q;
   c.k = k;
@@ -390,6 +417,8 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
   c.scale_log2 = softmax_scale * 1.4426950408889634f;
   c.d = d;
   c.fp32 = dtype == EVISEL_FP32;
+  c.segv = frame_pairs ? w.segv : nullptr;
+  c.lse2v = cues ? w.lse2v : nullptr;
   hipStream_t s = (hipStream_t)stream;
   const bool prof =
       g_prof.open && g_prof.used < g_prof.ev.size() / kProfEvents;
@@ -417,9 +446,37 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
       text_mass ? text_mass + (size_t)layer * P.hq * P.seqs.size() : nullptr,
       s);
   if (e != hipSuccess) return hip_fail(e, "evidence launch");
+  if (prof) prof_record(call, 4, s);
+  if (frame_pairs) {
+    e = evisel::launch_frame_pairs(
+        m->dp, w, frame_pairs + (size_t)layer * P.pairs.size(), s);
+    if (e != hipSuccess) return hip_fail(e, "frame pair launch");
+  }
+  if (intra_frame) {
+    const size_t nv = (size_t)P.layout.Nv;
+    e = evisel::launch_intra_frame(
+        m->dp, w, c, intra_frame + (size_t)layer * P.T * nv * nv, s);
+    if (e != hipSuccess) return hip_fail(e, "intra-frame launch");
+  }
   if (prof) {
-    prof_record(call, 4, s);
+    prof_record(call, 5, s);
     g_prof.used++;
+  }
+  return EVISEL_OK;
+}
+
+size_t evisel_cue_workspace(const evisel_mask* m, int32_t d) {
+  if (!m || (d != 64 && d != 128)) return 0;
+  return ws_layout(m->plan, d).cue_total;
+}
+
+evisel_status evisel_mask_export_pairs(const evisel_mask* m, int32_t* a,
+                                       int32_t* b) {
+  if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
+  const auto& pr = m->plan.pairs;
+  for (size_t i = 0; i < pr.size(); ++i) {
+    if (a) a[i] = pr[i].a;
+    if (b) b[i] = pr[i].b;
   }
   return EVISEL_OK;
 }
@@ -458,7 +515,9 @@ evisel_status evisel_frame_evidence(const evisel_mask* m,
                                     const float* evidence, int32_t n_layers,
                                     float* e_qf_layer, float* e_qf,
                                     const int32_t* k_per_seq,
-                                    int32_t* topk_idx, void* stream) {
+                                    int32_t* topk_idx,
+                                    const float* frame_pairs, float* e_ff,
+                                    void* stream) {
   evisel_status st = check_device(m);
   if (st != EVISEL_OK) return st;
   if (!evidence || !e_qf || n_layers < 1)
@@ -470,10 +529,17 @@ evisel_status evisel_frame_evidence(const evisel_mask* m,
       if (sq.n_frames > 65536)
         return fail(EVISEL_ERR_UNSUPPORTED,
                     "top-k supports at most 65536 frames per video");
+  if (e_ff && !frame_pairs)
+    return fail(EVISEL_ERR_INVALID_ARG, "e_ff needs frame_pairs");
   hipError_t e = evisel::launch_frame_evidence(m->dp, evidence, n_layers,
                                                e_qf_layer, e_qf, k_per_seq,
                                                topk_idx, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "frame evidence launch");
+  if (e_ff) {
+    e = evisel::launch_e_ff(m->dp, frame_pairs, n_layers, e_ff,
+                            (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "e_ff launch");
+  }
   return EVISEL_OK;
 }
 

@@ -449,9 +449,15 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const int trow = qb.aux + qrow - sq.textrow0;
   float* const seg_row = ws.seg + (size_t)h * pl.segtot + sq.segbase +
                          (size_t)trow * sq.n_frames - sq.frame0;
+  // Frame cues: visual rows also leave one log2 partial mass per (row, key
+  // frame) of every computed visual tile, at the tile's CSR position.
+  const bool vis_ff = ac.segv != nullptr && !is_text && qb.region == kVis;
+  const int fpt = kTile / pl.Nv;                    // frames per key tile
+  float* const segv_row =
+      vis_ff ? ac.segv + (size_t)h * pl.nnz * fpt * kTile + qrow : nullptr;
   auto tile_post = [&](f32x16 (&s)[2], const BlockDesc& cur, float ts,
-                       const EV_LDS char* vt) {
-    if (is_text) {
+                       const EV_LDS char* vt, int cpos) {
+    if (is_text || vis_ff) {
       const float mu = m_ref == neg_inf() ? 0.f : m_ref;
       if (cur.region == kVis) {
         // per 8-key group partial sums, completed across the lane pair
@@ -466,15 +472,17 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         for (int q = 0; q < 8; ++q) g8[q] = pair_sum(g8[q]);
         const int lg = __builtin_ctz((unsigned)pl.Nv) - 3;  // log2(N_v / 8)
         const int nseg = kTile / pl.Nv;
-        float* dst = seg_row + cur.aux;
+        float* dst = is_text ? seg_row + cur.aux
+                             : segv_row + (size_t)(b0 + cpos) * fpt * kTile;
+        const int dstride = is_text ? 1 : kTile;
         for (int si = 0; si < nseg; ++si) {
           float t = 0.f;
 #pragma unroll
           for (int q = 0; q < 8; ++q) t += (q >> lg) == si ? g8[q] : 0.f;
           if (g == 0 && qvalid && si * pl.Nv < cur.len)
-            dst[si] = mu + log2_(t);
+            dst[si * dstride] = mu + log2_(t);
         }
-      } else {
+      } else if (is_text) {
         nv_part += ts;
       }
     }
@@ -487,13 +495,15 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   // trips in front of every tile's K/V loads.)
   // Top-p: dsc_loc is the tile's local history index, or -1 when the tile
   // is always visible.
-  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1;
+  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1,
+      dsc_pos = 0;
   auto load_batch = [&](int batch) {
     const int t = batch * 64 + lane;
     if (t < n) {
       const int pos = TOPP ? (int)clist[t] : t;
       const int bid = pl.col[b0 + pos];
       const BlockDesc bd = pl.blocks[bid];
+      dsc_pos = pos;
       dsc_start = bd.start;
       dsc_len = bd.len;
       dsc_region = bd.region;
@@ -525,11 +535,14 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   auto loc_of = [&](int t) {
     return TOPP ? __builtin_amdgcn_readlane(dsc_loc, t & 63) : -1;
   };
+  auto pos_of = [&](int t) {   // CSR offset of compacted tile t
+    return TOPP ? __builtin_amdgcn_readlane(dsc_pos, t & 63) : t;
+  };
 
   // Tile j+1 streams into the other buffer pair while tile j is computed.
   load_batch(0);
   BlockDesc kb = desc(0);
-  int lnext = loc_of(0);
+  int lnext = loc_of(0), pnext = pos_of(0);
   unsigned wnext = 0u;
   if (n > 0) {
     kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
@@ -538,7 +551,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   }
   for (int j = 0; j < n; ++j) {
     const BlockDesc cur = kb;
-    const int lcur = lnext;
+    const int lcur = lnext, pcur = pnext;
     if (((j + 1) & 63) == 0 && j + 1 < n) load_batch((j + 1) >> 6);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const unsigned wcur = wnext;
@@ -551,13 +564,14 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         lnext = loc_of(j + 1);
         wnext = row_bits(lnext);
       }
+      pnext = pos_of(j + 1);
     }
     if (active) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
       P::qk(s, kbuf(j), qf, l32, g);
       tile_pre(s, cur, wcur, lcur);
       const float ts = tile_main(s);
-      tile_post(s, cur, ts, vbuf(j));
+      tile_post(s, cur, ts, vbuf(j), pcur);
     }
   }
   if (!active) return;
@@ -576,6 +590,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         }
       if (g == 0 && ac.lse)
         ac.lse[(size_t)h * pl.S + qpos] = (m_ref + log2_(l_tot)) * kLn2;
+      if (g == 0 && ac.lse2v)
+        ac.lse2v[(size_t)h * pl.S + qpos] = m_ref + log2_(l_tot);
     }
   } else {
     const float nv_tot = pair_sum(nv_part);
@@ -598,6 +614,86 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       }
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Intra-frame cue: per visual block, the head-averaged probabilities among
+// the tokens of each frame, P_im = exp2(s_im * scale - lse2_i) for key m <=
+// query i in i's frame (the block's diagonal tile, recomputed with the same
+// MFMA contraction as the attention pass and normalised by the row LSE it
+// saved). One work-group per block; the K tile of each kv head is staged in
+// LDS once; waves 0-1 take the even heads of each head pair, waves 2-3 the
+// odd ones, and the two partial sums are added in that fixed order.
+template <class P, int D>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads)))
+void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac,
+                  float* __restrict__ out) {
+  using T = typename P::T;
+  constexpr int TB = kTile * P::RC * 16;
+  constexpr int RB = 2 * 64 * 32 * 4;              // wave-pair hand-off
+  __shared__ __attribute__((aligned(1024))) char smem[TB > RB ? TB : RB];
+  EV_LDS char* kt = (EV_LDS char*)smem;
+  const BlockDesc qb = pl.blocks[blockIdx.x];
+  if (qb.region != kVis) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, g = lane >> 5;
+  const int qrow = 32 * (wave & 1) + l32;
+  const bool qvalid = qrow < qb.len;
+  const int qpos = qb.start + qrow;
+  const int Nv = pl.Nv;
+  const int group = pl.hq / pl.hkv;
+  const float c2 = ac.scale_log2;
+  TileLoader<T, D, kSwzK> kload;
+  kload.init(pl.hkv, wave, lane);
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
+  for (int kvh = 0; kvh < pl.hkv; ++kvh) {
+    __syncthreads();                    // previous K tile fully consumed
+    kload.issue(kt, (const T*)ac.k, qb.start, qb.len, kvh, wave);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int hp = 0; hp < group; hp += 2) {
+      const int h = kvh * group + hp + (wave >> 1);
+      if (hp + (wave >> 1) >= group) continue;   // odd group: no partner
+      typename P::QFrag qf;
+      P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
+      f32x16 s[2] = {f32x16{}, f32x16{}};
+      P::qk(s, kt, qf, l32, g);
+      const float l2 = qvalid ? ws.lse2v[(size_t)h * pl.S + qpos] : 0.f;
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
+          const bool ok = qvalid && kl <= qrow && kl / Nv == qrow / Nv;
+          acc[c][r] += ok ? exp2_(fmaf(s[c][r], c2, -l2)) : 0.f;
+        }
+    }
+  }
+  // waves 2-3 hand their sums to waves 0-1 through LDS
+  __syncthreads();
+  float* red = (float*)smem;                       // [2][64 lanes][32]
+  if (wave >= 2) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[((wave & 1) * 64 + lane) * 32 + 16 * c + r] = acc[c][r];
+  }
+  __syncthreads();
+  if (wave >= 2 || !qvalid) return;
+  const float inv = 1.f / (float)pl.hq;
+  const int fr = qrow / Nv, ii = qrow % Nv;
+  float* dst = out + ((size_t)(qb.aux + fr) * Nv + ii) * Nv;
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
+      if (kl / Nv != fr || kl >= qb.len) continue;
+      const float v = acc[c][r] + red[((wave & 1) * 64 + lane) * 32 + 16 * c + r];
+      dst[kl % Nv] = v * inv;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -701,6 +797,23 @@ hipError_t launch_attention(const DevPlan& p, const Workspace& w,
       attn_kernel<Bf16Path<64>, 64, false><<<grid, block, 0, s>>>(p, w, c);
     else
       attn_kernel<Bf16Path<128>, 128, false><<<grid, block, 0, s>>>(p, w, c);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_intra_frame(const DevPlan& p, const Workspace& w,
+                              const AttnCall& c, float* out, hipStream_t s) {
+  dim3 grid(p.nb), block(kThreads);
+  if (c.fp32) {
+    if (c.d == 64)
+      intra_kernel<F32Path<64>, 64><<<grid, block, 0, s>>>(p, w, c, out);
+    else
+      intra_kernel<F32Path<128>, 128><<<grid, block, 0, s>>>(p, w, c, out);
+  } else {
+    if (c.d == 64)
+      intra_kernel<Bf16Path<64>, 64><<<grid, block, 0, s>>>(p, w, c, out);
+    else
+      intra_kernel<Bf16Path<128>, 128><<<grid, block, 0, s>>>(p, w, c, out);
   }
   return hipGetLastError();
 }

@@ -128,7 +128,99 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
   }
 }
 
+// Cross-frame cue of one layer: one wavefront per frame pair (a, b). Lane r
+// < N_v owns row r of frame a; it adds, over the heads in order, the row's
+// normalised mass on frame b, exp2(partial - LSE), from the partial the
+// attention pass left for that key tile. A top-p tile that no row of head
+// h's work item kept was never computed and adds nothing. The lanes are
+// then summed by a butterfly (every lane ends with the same bits) and the
+// pair gets the mean over heads and frame a's rows.
+constexpr int kPairWaves = 4;
+
+__global__ __launch_bounds__(64 * kPairWaves) void frame_pairs_kernel(
+    const DevPlan pl, const Workspace ws, float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int pi = blockIdx.x * kPairWaves + (threadIdx.x >> 6);
+  if (pi >= pl.n_pairs) return;
+  const FramePair fp = pl.pairs[pi];
+  const int fpt = 64 / pl.Nv;
+  const BlockDesc qb = pl.blocks[fp.qblock];
+  const int kb = pl.col[fp.pos];
+  const int loc = pl.blk_local[kb];
+  const bool always = !pl.topp || kb == fp.qblock || loc < 0;
+  const int group = pl.hq / pl.hkv;
+  const bool rv = lane < pl.Nv;
+  const int row = fp.roff + (rv ? lane : 0);
+  float acc = 0.f;
+  for (int h = 0; h < pl.hq; ++h) {
+    bool done = always;
+    if (!always) {
+      const int g0 = (h / group) * group;
+      const int h0 = g0 + ((h - g0) / kHeadsPerItem) * kHeadsPerItem;
+      const int nh = min(kHeadsPerItem, g0 + group - h0);
+      unsigned wd = 0u;
+      for (int i = 0; i < nh; ++i)
+        wd |= ws.ubits[((size_t)(h0 + i) * pl.nb + fp.qblock) * pl.W +
+                       (loc >> 5)];
+      done = (wd >> (loc & 31)) & 1u;
+    }
+    if (done && rv) {
+      const float sv =
+          ws.segv[(((size_t)h * pl.nnz + fp.pos) * fpt + fp.koff) * 64 + row];
+      const float l2 = ws.lse2v[(size_t)h * pl.S + qb.start + row];
+      acc += exp2_(sv - l2);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) out[pi] = acc / ((float)pl.hq * (float)pl.Nv);
+}
+
+// E_ff[l, t]: the mean over t's earlier frames of A_ff[t, b] and the mean
+// over its later frames of A_ff[a, t], averaged over the sides that exist
+// (pairs outside the sparse pattern are 0). Fixed summation order.
+__global__ __launch_bounds__(256) void e_ff_kernel(const DevPlan pl,
+                                                   const float* __restrict__ pr,
+                                                   float* __restrict__ e_ff) {
+  const int t = blockIdx.x * 256 + threadIdx.x, l = blockIdx.y;
+  if (t >= pl.T) return;
+  const SeqDesc sq = pl.seqs[pl.frame_seq[t]];
+  const int tl = t - sq.frame0, F = sq.n_frames;
+  const float* p = pr + (size_t)l * pl.n_pairs;
+  float o = 0.f, in = 0.f;
+  for (int i = pl.ff_out_ptr[t]; i < pl.ff_out_ptr[t + 1]; ++i)
+    o += p[pl.ff_out_idx[i]];
+  for (int i = pl.ff_in_ptr[t]; i < pl.ff_in_ptr[t + 1]; ++i)
+    in += p[pl.ff_in_idx[i]];
+  float acc = 0.f;
+  int ns = 0;
+  if (tl > 0) {
+    acc += o / (float)tl;
+    ++ns;
+  }
+  if (tl < F - 1) {
+    acc += in / (float)(F - 1 - tl);
+    ++ns;
+  }
+  e_ff[(size_t)l * pl.T + t] = ns ? acc / (float)ns : 0.f;
+}
+
 }  // namespace
+
+hipError_t launch_frame_pairs(const DevPlan& p, const Workspace& w,
+                              float* pairs_out, hipStream_t s) {
+  if (p.n_pairs == 0) return hipSuccess;
+  frame_pairs_kernel<<<dim3((p.n_pairs + kPairWaves - 1) / kPairWaves),
+                       dim3(64 * kPairWaves), 0, s>>>(p, w, pairs_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_e_ff(const DevPlan& p, const float* pairs,
+                       int32_t n_layers, float* e_ff, hipStream_t s) {
+  e_ff_kernel<<<dim3((p.T + 255) / 256, n_layers), dim3(256), 0, s>>>(
+      p, pairs, e_ff);
+  return hipGetLastError();
+}
 
 hipError_t launch_evidence(const DevPlan& p, const Workspace& w, float* ev,
                            float* tm, hipStream_t s) {

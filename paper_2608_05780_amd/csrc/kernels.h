@@ -15,6 +15,13 @@ struct DevPlan {
   const TextTile* tiles;
   const int32_t* frame_seq;
   const int32_t* blk_local;  // [nb] local selectable index, -1 for system
+  const FramePair* pairs;    // [n_pairs] cross-frame pairs
+  const int32_t* ff_out_ptr; // [T+1] pairs whose query frame is t
+  const int32_t* ff_out_idx;
+  const int32_t* ff_in_ptr;  // [T+1] pairs whose key frame is t
+  const int32_t* ff_in_idx;
+  int32_t n_pairs;
+  int32_t nnz;               // CSR entries
   int32_t n_items, n_tiles, n_seq;
   int32_t S, T, n_text_rows;
   int64_t segtot;
@@ -38,6 +45,10 @@ struct Workspace {
   void* kbar;              // bf16: hi [hkv][nb][d] then lo; fp32: [hkv][nb][d]
   uint32_t* rbits;         // [hq][nb][W][64] retained history per row
   uint32_t* ubits;         // [hq][nb][W]     union over the block's rows
+  // frame cues (null unless requested)
+  float* segv;             // [hq][nnz][64 / N_v][64] log2 partial mass of a
+                           // visual row on each frame of a computed key tile
+  float* lse2v;            // [hq][S] log2 LSE of visual rows
 };
 
 struct SelCall {
@@ -60,6 +71,8 @@ struct AttnCall {
   float scale_log2;      // softmax scale * log2(e)
   int32_t d;
   int32_t fp32;          // 1: fp32 inputs/outputs, 0: bf16
+  float* segv;           // frame-cue partials of visual rows, or null
+  float* lse2v;          // visual rows' log2 LSE, or null
 };
 
 hipError_t launch_attention(const DevPlan& p, const Workspace& w,
@@ -83,5 +96,14 @@ hipError_t launch_frame_evidence(const DevPlan& p, const float* evidence,
                                  int32_t n_layers, float* e_qf_layer,
                                  float* e_qf, const int32_t* k_per_seq,
                                  int32_t* topk, hipStream_t s);
+// Cross-frame cue of one layer: pairs_out[i] = A_ff of pair i.
+hipError_t launch_frame_pairs(const DevPlan& p, const Workspace& w,
+                              float* pairs_out, hipStream_t s);
+// Intra-frame cue of one layer: out [T][N_v][N_v].
+hipError_t launch_intra_frame(const DevPlan& p, const Workspace& w,
+                              const AttnCall& c, float* out, hipStream_t s);
+// E_ff [n_layers][T] from the cross-frame pairs [n_layers][n_pairs].
+hipError_t launch_e_ff(const DevPlan& p, const float* pairs,
+                       int32_t n_layers, float* e_ff, hipStream_t s);
 
 }  // namespace evisel

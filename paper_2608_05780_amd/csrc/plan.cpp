@@ -147,6 +147,45 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   // bits for history blocks 0 .. max_sel - 2
   P.hist_words = std::max(1, (max_sel - 1 + 31) / 32);
 
+  // ---- frame pairs of the cross-frame cue ---------------------------------
+  for (size_t n = 0; n < nseq; ++n) {
+    const int64_t vis0 = P.seqs[n].vis0, frame0 = P.seqs[n].frame0;
+    for (int32_t qb : visb[n]) {
+      const BlockDesc& q = P.blocks[qb];
+      const int32_t fa0 = (int32_t)((q.start - vis0) / L.Nv);
+      const int32_t fa1 = (int32_t)((q.start + q.len - 1 - vis0) / L.Nv);
+      for (int32_t p = P.row_ptr[qb]; p < P.row_ptr[qb + 1]; ++p) {
+        const BlockDesc& k = P.blocks[P.col[p]];
+        if (k.region != kVis) continue;
+        const int32_t fb0 = (int32_t)((k.start - vis0) / L.Nv);
+        const int32_t fb1 = (int32_t)((k.start + k.len - 1 - vis0) / L.Nv);
+        for (int32_t fa = fa0; fa <= fa1; ++fa)
+          for (int32_t fb = fb0; fb <= fb1 && fb < fa; ++fb) {
+            FramePair fp;
+            fp.pos = p;
+            fp.a = (int32_t)(frame0 + fa);
+            fp.b = (int32_t)(frame0 + fb);
+            fp.qblock = qb;
+            fp.roff = (int32_t)(vis0 + (int64_t)fa * L.Nv - q.start);
+            fp.koff = fb - fb0;
+            P.pairs.push_back(fp);
+          }
+      }
+    }
+  }
+  auto index_by = [&](bool by_a, std::vector<int32_t>& ptr,
+                      std::vector<int32_t>& idx) {
+    ptr.assign(P.T + 1, 0);
+    for (const FramePair& fp : P.pairs) ptr[(by_a ? fp.a : fp.b) + 1]++;
+    for (int64_t t = 0; t < P.T; ++t) ptr[t + 1] += ptr[t];
+    idx.assign(P.pairs.size(), 0);
+    std::vector<int32_t> fill(ptr.begin(), ptr.end() - 1);
+    for (size_t i = 0; i < P.pairs.size(); ++i)
+      idx[fill[by_a ? P.pairs[i].a : P.pairs[i].b]++] = (int32_t)i;
+  };
+  index_by(true, P.ff_out_ptr, P.ff_out_idx);
+  index_by(false, P.ff_in_ptr, P.ff_in_idx);
+
   // ---- work items ---------------------------------------------------------
   const int32_t group = hq / hkv;
   const int32_t pairs = (group + kHeadsPerItem - 1) / kHeadsPerItem;

@@ -60,6 +60,17 @@ struct TextTile {
   int32_t slot0;
 };
 
+// A (query frame, earlier key frame) pair of one video that the sparse
+// pattern can connect (cross-frame cue): the key frame lies in the key tile
+// at CSR position `pos` of the query frame's block.
+struct FramePair {
+  int32_t pos;      // CSR position (query block row, key tile)
+  int32_t a, b;     // global query and key frame, b < a
+  int32_t qblock;   // block holding frame a's rows
+  int32_t roff;     // first row of frame a within qblock
+  int32_t koff;     // frame index of b within the key tile
+};
+
 struct Layout {
   std::vector<int32_t> n_sys, n_frames, n_text;
   int32_t Nv = 0;
@@ -100,6 +111,10 @@ struct Plan {
   std::vector<int32_t> blk_local;
   int32_t hist_words = 0;
   int32_t max_item_candidates = 0;
+  // cross-frame cue: every connectable frame pair, and per frame the pairs
+  // where it is the query frame (out) and the key frame (in), in pair order
+  std::vector<FramePair> pairs;
+  std::vector<int32_t> ff_out_ptr, ff_out_idx, ff_in_ptr, ff_in_idx;
 };
 
 // Builds the plan; returns "" on success or an error message.

@@ -25,6 +25,9 @@ class GpuRun:
     e_qf_layer: np.ndarray
     topk: list       # per video int arrays (local frame ids)
     mask: object
+    pairs: object = None      # [L, n_pairs] A_ff of the exported pairs
+    intra: object = None      # [L, T, N_v, N_v] A_if
+    e_ff: object = None       # [L, T]
 
 
 def to_device(layer: wl.Layer, w: wl.Workload, torch):
@@ -37,7 +40,7 @@ def to_device(layer: wl.Layer, w: wl.Workload, torch):
 
 
 def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
-            keep_o=True, layer_inputs=None, on_layer=None):
+            keep_o=True, layer_inputs=None, on_layer=None, cues=False):
     """Run ``layers`` (list of layer ids) of workload ``w`` on the GPU.
 
     ``on_layer(j, layer_id, out, lse)`` (torch tensors on the GPU) is called
@@ -55,15 +58,22 @@ def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
     lse = torch.empty((w.hq, S), dtype=torch.float32, device="cuda")
     evid = torch.full((L, w.hq, T), float("nan"), device="cuda")
     tm = torch.full((L, w.hq, nseq), float("nan"), device="cuda")
-    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d), dtype=torch.uint8,
-                     device="cuda")
+    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d, cues=cues),
+                     dtype=torch.uint8, device="cuda")
+    pairs = intra = None
+    if cues:
+        npair = st["n_frame_pairs"]
+        pairs = torch.full((L, max(npair, 1)), float("nan"), device="cuda")
+        intra = torch.full((L, T, w.tokens_per_frame, w.tokens_per_frame),
+                           float("nan"), device="cuda")
     Os, LSEs = [], []
     for j, l in enumerate(layers):
         lay = layer_inputs(l) if layer_inputs else wl.gen_layer(w, l, seed)
         q, k, v = to_device(lay, w, torch)
         say(f"  gpu: {w.name} layer {l} S={S} hq={w.hq} d={w.d}")
         ev.sparse_prefill(mask, j, L, q, k, v, out, evid, ws, lse=lse,
-                          text_mass=tm, softmax_scale=w.softmax_scale)
+                          text_mass=tm, softmax_scale=w.softmax_scale,
+                          frame_pairs=pairs, intra_frame=intra)
         torch.cuda.synchronize()
         if on_layer is not None:
             on_layer(j, l, out, lse)
@@ -88,10 +98,19 @@ def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
     else:
         ev.frame_evidence(mask, evid, L, e_qf, e_qf_layer=e_qf_layer)
         torch.cuda.synchronize()
+    e_ff = None
+    if cues:
+        e_ff = torch.full((L, T), float("nan"), device="cuda")
+        ev.frame_evidence(mask, evid, L, e_qf, frame_pairs=pairs, e_ff=e_ff)
+        torch.cuda.synchronize()
+        e_ff = e_ff.cpu().numpy().astype(np.float64)
+        pairs = pairs.cpu().numpy().astype(np.float64)[:, :st["n_frame_pairs"]]
+        intra = intra.cpu().numpy().astype(np.float64)
     return GpuRun(Os, LSEs, evid.cpu().numpy().astype(np.float64),
                   tm.cpu().numpy().astype(np.float64),
                   e_qf.cpu().numpy().astype(np.float64),
-                  e_qf_layer.cpu().numpy().astype(np.float64), topk, mask)
+                  e_qf_layer.cpu().numpy().astype(np.float64), topk, mask,
+                  pairs, intra, e_ff)
 
 
 def sample_rows(lay, n_rows, seed, run=64):

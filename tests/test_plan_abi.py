@@ -168,11 +168,12 @@ def test_error_codes(lib):
     # compute calls refuse a host-only plan before touching the device
     m = _plan([3], [2], 64, r)
     st = lib.evisel_sparse_prefill(m.handle, 0, 1, None, None, None, 128, 0,
-                                   0.1, None, None, None, None, None, 0, None)
+                                   0.1, None, None, None, None, None, None,
+                                   None, 0, None)
     assert st == ev.ERR_INVALID_ARG
     assert b"device" in lib.evisel_last_error()
     st = lib.evisel_frame_evidence(m.handle, None, 1, None, None, None, None,
-                                   None)
+                                   None, None, None)
     assert st == ev.ERR_INVALID_ARG
     assert lib.evisel_sparse_prefill_workspace(m.handle, 96) == 0
     assert lib.evisel_sparse_prefill_workspace(m.handle, 128) > 0
