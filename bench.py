@@ -97,6 +97,23 @@ def topp_computed_pairs(ev, mask, w, qs, kks, ws):
     return total / len(qs), kept / max(hist, 1.0)
 
 
+def cue_record(w, st, S, T, prof):
+    """Frame-cue kernels per layer: their HIP-event time and the bytes the
+    two kernels must move at least (the intra-frame pass reads the visual
+    rows' Q, the K of their blocks and their LSE and writes the maps; the
+    pair pass reads one partial and one LSE per (head, pair row))."""
+    Nv, calls = w.tokens_per_frame, max(1, prof["calls"])
+    s_vis = T * Nv
+    esz = 2 if w.dtype == "bf16" else 4
+    intra_bytes = (s_vis * (w.hq + w.hkv) * w.d * esz + w.hq * s_vis * 4 +
+                   T * Nv * Nv * 4)
+    pair_bytes = st["n_frame_pairs"] * w.hq * Nv * 8 + st["n_frame_pairs"] * 4
+    ms = prof["cues_ms"] / calls
+    return {"ms_per_layer": ms, "frame_pairs": st["n_frame_pairs"],
+            "algorithmic_bytes_per_layer": intra_bytes + pair_bytes,
+            "achieved_GBps": (intra_bytes + pair_bytes) / (ms * 1e-3) / 1e9}
+
+
 def _world():
     return int(os.environ.get("WORLD_SIZE", "1")), int(os.environ.get("RANK",
                                                                       "0"))
@@ -138,6 +155,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cues", action="store_true",
+                    help="also produce the cross-frame (A_ff, E_ff) and "
+                         "intra-frame (A_if) cues in every step")
     ap.add_argument("--tau-p", type=float, default=0.0,
                     help="adaptive top-p retention threshold (0: the "
                          "workload's static rule)")
@@ -210,17 +230,26 @@ def main():
     e_qf = torch.empty(T, dtype=torch.float32, device="cuda")
     kk = torch.tensor(ks, dtype=torch.int32, device="cuda")
     topk = torch.empty(max(1, sum(ks)), dtype=torch.int32, device="cuda")
-    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d), dtype=torch.uint8,
-                     device="cuda")
+    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d, cues=args.cues),
+                     dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    pairs = intra = e_ff = None
+    if args.cues:
+        Nv = w.tokens_per_frame
+        pairs = torch.empty((L, max(1, st["n_frame_pairs"])),
+                            dtype=torch.float32, device="cuda")
+        intra = torch.empty((L, T, Nv, Nv), dtype=torch.float32,
+                            device="cuda")
+        e_ff = torch.empty((L, T), dtype=torch.float32, device="cuda")
 
     def step():
         for l in range(L):
             ev.sparse_prefill(mask, l, L, qs[l], kks[l], vs[l], out, evid, ws,
                               lse=lse, text_mass=tmass,
-                              softmax_scale=w.softmax_scale, stream=stream)
+                              softmax_scale=w.softmax_scale, stream=stream,
+                              frame_pairs=pairs, intra_frame=intra)
         ev.frame_evidence(mask, evid, L, e_qf, k_per_seq=kk, topk=topk,
-                          stream=stream)
+                          stream=stream, frame_pairs=pairs, e_ff=e_ff)
 
     for _ in range(args.warmup):
         step()
@@ -275,11 +304,13 @@ def main():
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms},
         "kernels_ms_per_layer": {
+            "cues": prof["cues_ms"] / max(1, prof["calls"]),
             "retention": prof["select_ms"] / max(1, prof["calls"]),
             "attention": attn_ms,
             "combine": prof["combine_ms"] / max(1, prof["calls"]),
             "evidence": ev_ms},
         "evidence_reduce_GBps": ev_bytes / (ev_ms * 1e-3) / 1e9,
+        **({"cues": cue_record(w, st, S, T, prof)} if args.cues else {}),
         "topk_planted_recovered": planted_ok,
     }
     if w.tau_p > 0:

@@ -147,7 +147,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
 
 struct WsLayout {
   size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, total;
-  size_t segv, lse2v, cue_total;   // frame cues, after `total`
+  size_t segv, lse2v, intra_part, cue_total;   // frame cues, after `total`
 };
 
 WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
@@ -180,6 +180,7 @@ WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
                       ? 64 / P.layout.Nv : 1;
   w.segv = take((size_t)P.hq * P.col.size() * fpt * 64 * 4);
   w.lse2v = take((size_t)P.hq * P.S * 4);
+  w.intra_part = take((size_t)P.hkv * P.T * P.layout.Nv * P.layout.Nv * 4);
   w.cue_total = off - w.total;
   return w;
 }
@@ -202,6 +203,7 @@ evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp,
   w.ubits = topp ? (uint32_t*)(wb + wl.ubits) : nullptr;
   w.segv = cues ? (float*)(wb + wl.segv) : nullptr;
   w.lse2v = cues ? (float*)(wb + wl.lse2v) : nullptr;
+  w.intra_part = cues ? (float*)(wb + wl.intra_part) : nullptr;
   return w;
 }
 

@@ -43,6 +43,8 @@
 // split into chunks of key blocks (longest-first balance across the chip);
 // each chunk leaves an unnormalised partial (acc, m_ref, row sum, non-visual
 // mass) in the workspace and the combine kernel merges them.
+#include <algorithm>
+
 #include "kernels.h"
 
 #define EV_LDS __attribute__((address_space(3)))
@@ -459,7 +461,13 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
                        const EV_LDS char* vt, int cpos) {
     if (is_text || vis_ff) {
       const float mu = m_ref == neg_inf() ? 0.f : m_ref;
-      if (cur.region == kVis) {
+      if (cur.region == kVis && pl.Nv == kTile) {
+        // one frame per key tile: its partial is the row's tile sum
+        float* dst = is_text ? seg_row + cur.aux
+                             : segv_row + (size_t)(b0 + cpos) * kTile;
+        const float t = pair_sum(ts);
+        if (g == 0 && qvalid) *dst = mu + log2_(t);
+      } else if (cur.region == kVis) {
         // per 8-key group partial sums, completed across the lane pair
         float g8[8];
 #pragma unroll
@@ -617,17 +625,19 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 }
 
 // ---------------------------------------------------------------------------
-// Intra-frame cue: per visual block, the head-averaged probabilities among
+// Intra-frame cue: per visual block and kv head, the probabilities among
 // the tokens of each frame, P_im = exp2(s_im * scale - lse2_i) for key m <=
 // query i in i's frame (the block's diagonal tile, recomputed with the same
 // MFMA contraction as the attention pass and normalised by the row LSE it
-// saved). One work-group per block; the K tile of each kv head is staged in
+// saved), summed over the kv head's query heads. The K tile is staged in
 // LDS once; waves 0-1 take the even heads of each head pair, waves 2-3 the
-// odd ones, and the two partial sums are added in that fixed order.
+// odd ones, the next pair's Q and LSE are fetched while the current pair is
+// computed, and the two wave groups' sums are added in a fixed order. The
+// result is a partial per kv head; intra_reduce_kernel adds the kv heads in
+// order and divides by Hq.
 template <class P, int D>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads)))
-void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac,
-                  float* __restrict__ out) {
+void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   using T = typename P::T;
   constexpr int TB = kTile * P::RC * 16;
   constexpr int RB = 2 * 64 * 32 * 4;              // wave-pair hand-off
@@ -635,6 +645,7 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac,
   EV_LDS char* kt = (EV_LDS char*)smem;
   const BlockDesc qb = pl.blocks[blockIdx.x];
   if (qb.region != kVis) return;
+  const int kvh = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, g = lane >> 5;
@@ -643,32 +654,46 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac,
   const int qpos = qb.start + qrow;
   const int Nv = pl.Nv;
   const int group = pl.hq / pl.hkv;
+  const int npair = (group + 1) / 2;
   const float c2 = ac.scale_log2;
   TileLoader<T, D, kSwzK> kload;
   kload.init(pl.hkv, wave, lane);
+  kload.issue(kt, (const T*)ac.k, qb.start, qb.len, kvh, wave);
+
   f32x16 acc[2] = {f32x16{}, f32x16{}};
-  for (int kvh = 0; kvh < pl.hkv; ++kvh) {
-    __syncthreads();                    // previous K tile fully consumed
-    kload.issue(kt, (const T*)ac.k, qb.start, qb.len, kvh, wave);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    for (int hp = 0; hp < group; hp += 2) {
-      const int h = kvh * group + hp + (wave >> 1);
-      if (hp + (wave >> 1) >= group) continue;   // odd group: no partner
-      typename P::QFrag qf;
-      P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
-      f32x16 s[2] = {f32x16{}, f32x16{}};
-      P::qk(s, kt, qf, l32, g);
-      const float l2 = qvalid ? ws.lse2v[(size_t)h * pl.S + qpos] : 0.f;
+  // head of pair pi for this wave (or -1 past an odd group's end)
+  auto head = [&](int pi) {
+    const int hi = 2 * pi + (wave >> 1);
+    return pi < npair && hi < group ? kvh * group + hi : -1;
+  };
+  auto fetch = [&](typename P::QFrag& qf, float& l2, int h) {
+    if (h < 0) return;
+    P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
+    l2 = qvalid ? ws.lse2v[(size_t)h * pl.S + qpos] : 0.f;
+  };
+  auto accumulate = [&](const typename P::QFrag& qf, float l2, int h) {
+    if (h < 0) return;
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+    P::qk(s, kt, qf, l32, g);
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
-          const bool ok = qvalid && kl <= qrow && kl / Nv == qrow / Nv;
-          acc[c][r] += ok ? exp2_(fmaf(s[c][r], c2, -l2)) : 0.f;
-        }
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
+        const bool ok = qvalid && kl <= qrow && kl / Nv == qrow / Nv;
+        acc[c][r] += ok ? exp2_(fmaf(s[c][r], c2, -l2)) : 0.f;
+      }
+  };
+  typename P::QFrag qa, qb2;
+  float la = 0.f, lb = 0.f;
+  fetch(qa, la, head(0));
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();                                 // K tile in LDS
+  for (int pi = 0; pi < npair; pi += 2) {
+    fetch(qb2, lb, head(pi + 1));
+    accumulate(qa, la, head(pi));
+    fetch(qa, la, head(pi + 2));
+    accumulate(qb2, lb, head(pi + 1));
   }
   // waves 2-3 hand their sums to waves 0-1 through LDS
   __syncthreads();
@@ -682,18 +707,30 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac,
   }
   __syncthreads();
   if (wave >= 2 || !qvalid) return;
-  const float inv = 1.f / (float)pl.hq;
   const int fr = qrow / Nv, ii = qrow % Nv;
-  float* dst = out + ((size_t)(qb.aux + fr) * Nv + ii) * Nv;
+  float* dst = ws.intra_part +
+               (((size_t)kvh * pl.T + qb.aux + fr) * Nv + ii) * Nv;
 #pragma unroll
   for (int c = 0; c < 2; ++c)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
       if (kl / Nv != fr || kl >= qb.len) continue;
-      const float v = acc[c][r] + red[((wave & 1) * 64 + lane) * 32 + 16 * c + r];
-      dst[kl % Nv] = v * inv;
+      dst[kl % Nv] =
+          acc[c][r] + red[((wave & 1) * 64 + lane) * 32 + 16 * c + r];
     }
+}
+
+__global__ __launch_bounds__(256) void intra_reduce_kernel(
+    const DevPlan pl, const Workspace ws, float* __restrict__ out) {
+  const size_t n = (size_t)pl.T * pl.Nv * pl.Nv;
+  const float inv = 1.f / (float)pl.hq;
+  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < n;
+       e += (size_t)gridDim.x * 256) {
+    float t = 0.f;
+    for (int kvh = 0; kvh < pl.hkv; ++kvh) t += ws.intra_part[kvh * n + e];
+    out[e] = t * inv;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -803,18 +840,23 @@ hipError_t launch_attention(const DevPlan& p, const Workspace& w,
 
 hipError_t launch_intra_frame(const DevPlan& p, const Workspace& w,
                               const AttnCall& c, float* out, hipStream_t s) {
-  dim3 grid(p.nb), block(kThreads);
+  dim3 grid(p.nb, p.hkv), block(kThreads);
   if (c.fp32) {
     if (c.d == 64)
-      intra_kernel<F32Path<64>, 64><<<grid, block, 0, s>>>(p, w, c, out);
+      intra_kernel<F32Path<64>, 64><<<grid, block, 0, s>>>(p, w, c);
     else
-      intra_kernel<F32Path<128>, 128><<<grid, block, 0, s>>>(p, w, c, out);
+      intra_kernel<F32Path<128>, 128><<<grid, block, 0, s>>>(p, w, c);
   } else {
     if (c.d == 64)
-      intra_kernel<Bf16Path<64>, 64><<<grid, block, 0, s>>>(p, w, c, out);
+      intra_kernel<Bf16Path<64>, 64><<<grid, block, 0, s>>>(p, w, c);
     else
-      intra_kernel<Bf16Path<128>, 128><<<grid, block, 0, s>>>(p, w, c, out);
+      intra_kernel<Bf16Path<128>, 128><<<grid, block, 0, s>>>(p, w, c);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t n = (size_t)p.T * p.Nv * p.Nv;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  intra_reduce_kernel<<<dim3(blocks), dim3(256), 0, s>>>(p, w, out);
   return hipGetLastError();
 }
 

@@ -178,20 +178,30 @@ __global__ __launch_bounds__(64 * kPairWaves) void frame_pairs_kernel(
 
 // E_ff[l, t]: the mean over t's earlier frames of A_ff[t, b] and the mean
 // over its later frames of A_ff[a, t], averaged over the sides that exist
-// (pairs outside the sparse pattern are 0). Fixed summation order.
-__global__ __launch_bounds__(256) void e_ff_kernel(const DevPlan pl,
-                                                   const float* __restrict__ pr,
-                                                   float* __restrict__ e_ff) {
-  const int t = blockIdx.x * 256 + threadIdx.x, l = blockIdx.y;
+// (pairs outside the sparse pattern are 0). One wavefront per (layer,
+// frame): lanes take strided pairs, then a butterfly adds the lanes (fixed
+// order, every lane ends with the same bits).
+constexpr int kEffWaves = 4;
+
+__global__ __launch_bounds__(64 * kEffWaves) void e_ff_kernel(
+    const DevPlan pl, const float* __restrict__ pr, float* __restrict__ e_ff) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * kEffWaves + (threadIdx.x >> 6), l = blockIdx.y;
   if (t >= pl.T) return;
   const SeqDesc sq = pl.seqs[pl.frame_seq[t]];
   const int tl = t - sq.frame0, F = sq.n_frames;
   const float* p = pr + (size_t)l * pl.n_pairs;
   float o = 0.f, in = 0.f;
-  for (int i = pl.ff_out_ptr[t]; i < pl.ff_out_ptr[t + 1]; ++i)
+  for (int i = pl.ff_out_ptr[t] + lane; i < pl.ff_out_ptr[t + 1]; i += 64)
     o += p[pl.ff_out_idx[i]];
-  for (int i = pl.ff_in_ptr[t]; i < pl.ff_in_ptr[t + 1]; ++i)
+  for (int i = pl.ff_in_ptr[t] + lane; i < pl.ff_in_ptr[t + 1]; i += 64)
     in += p[pl.ff_in_idx[i]];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    o += __shfl_xor(o, m);
+    in += __shfl_xor(in, m);
+  }
+  if (lane) return;
   float acc = 0.f;
   int ns = 0;
   if (tl > 0) {
@@ -217,8 +227,8 @@ hipError_t launch_frame_pairs(const DevPlan& p, const Workspace& w,
 
 hipError_t launch_e_ff(const DevPlan& p, const float* pairs,
                        int32_t n_layers, float* e_ff, hipStream_t s) {
-  e_ff_kernel<<<dim3((p.T + 255) / 256, n_layers), dim3(256), 0, s>>>(
-      p, pairs, e_ff);
+  e_ff_kernel<<<dim3((p.T + kEffWaves - 1) / kEffWaves, n_layers),
+                dim3(64 * kEffWaves), 0, s>>>(p, pairs, e_ff);
   return hipGetLastError();
 }
 

@@ -49,6 +49,7 @@ struct Workspace {
   float* segv;             // [hq][nnz][64 / N_v][64] log2 partial mass of a
                            // visual row on each frame of a computed key tile
   float* lse2v;            // [hq][S] log2 LSE of visual rows
+  float* intra_part;       // [hkv][T][N_v][N_v] intra-frame sums per kv head
 };
 
 struct SelCall {
