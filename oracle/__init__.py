@@ -28,11 +28,14 @@ What it computes (each function cites the passage it follows):
                    Prefilling").
 * ``cues``      -- the cross-frame cue A_ff and its timestamp-aligned E_ff,
                    and the intra-frame cue A_if (Evidence Decomposition).
+* ``coarse``    -- the paper's coarse map (block affinity on retained blocks,
+                   exact logits on E_i; appendix, coarse-map equation) and the
+                   sparse-vs-dense alignment metrics.
 
 Parity pins live in ``tests/`` (brute force, closed forms, a library attention
 routine, invariants, planted ranking). No function here is "parity unpinned".
 """
-from . import layout, attention, aggregate, blocks, brute, topp, cues  # noqa: F401
+from . import layout, attention, aggregate, blocks, brute, topp, cues, coarse  # noqa: F401
 from .layout import Layout, Rule  # noqa: F401
 from .attention import run_layer, attend  # noqa: F401
 from .aggregate import frame_evidence, topk_per_video  # noqa: F401
