@@ -164,6 +164,26 @@ size_t evisel_cue_workspace(const evisel_mask* mask, int32_t d);
 evisel_status evisel_mask_export_pairs(const evisel_mask* mask, int32_t* a,
                                        int32_t* b);
 
+/* The paper's coarse query-frame evidence of one layer (appendix,
+ * coarse-map equation; top-p masks only). For each query token i the tokens
+ * of every retained history block j share the logit g_ij (the block
+ * affinity of the retention step), the tokens of E_i (the video's system
+ * prefix and the causal prefix of i's block) keep their exact logits
+ * q_i . k_m * softmax_scale, and the row is normalised over both.
+ *   evidence   device [Hq, T] fp32: per head and frame, the sum over the
+ *              video's query tokens of that coarse probability on the
+ *              frame's visual tokens (the coarse counterpart of
+ *              evisel_sparse_prefill's evidence slice)
+ * The call runs the retention itself (as evisel_select_blocks, into the
+ * workspace) and then the coarse pass; no attention output is formed.
+ * Errors: INVALID_ARG (static or host-only mask, NULL or misaligned
+ * pointer), UNSUPPORTED (d, dtype, B), WORKSPACE, HIP. */
+evisel_status evisel_coarse_evidence(const evisel_mask* mask, const void* q,
+                                     const void* k, int32_t d,
+                                     evisel_dtype dtype, float softmax_scale,
+                                     float* evidence, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
 /* Top-p retention of one layer alone (appendix, mean-key, affinity and
  * probability equations and the smallest subset reaching tau_p; see
  * evisel_mask_rule). evisel_sparse_prefill runs the same kernels itself;

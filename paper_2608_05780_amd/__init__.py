@@ -21,6 +21,7 @@ from typing import Optional, Sequence
 __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "sparse_prefill_workspace", "sparse_prefill", "frame_evidence",
            "select_blocks", "unpack_row_bits", "mask_export_pairs",
+           "coarse_evidence",
            "mask_info", "mask_export", "mask_export_work", "profile_begin",
            "profile_end", "LIB_PATH"]
 
@@ -85,6 +86,10 @@ _SIGS = {
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
         ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "evisel_coarse_evidence": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_size_t, ctypes.c_void_p]),
     "evisel_frame_evidence": (ctypes.c_int, [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -285,6 +290,19 @@ def select_blocks(mask: Mask, q, k, row_bits, block_bits, workspace,
     _check(load().evisel_select_blocks(
         mask.handle, _ptr(q), _ptr(k), d, _dtype_code(q), scale,
         _ptr(row_bits), _ptr(block_bits), _ptr(workspace),
+        0 if workspace is None else workspace.numel() * workspace.element_size(),
+        _stream(stream)))
+
+
+def coarse_evidence(mask: Mask, q, k, evidence, workspace,
+                    softmax_scale: Optional[float] = None, stream=None):
+    """The paper's coarse query-frame evidence of one layer (top-p masks):
+    ``evidence`` is a device fp32 tensor [Hq, T]."""
+    d = int(q.shape[-1])
+    scale = float(softmax_scale) if softmax_scale is not None else d ** -0.5
+    _check(load().evisel_coarse_evidence(
+        mask.handle, _ptr(q), _ptr(k), d, _dtype_code(q), scale,
+        _ptr(evidence), _ptr(workspace),
         0 if workspace is None else workspace.numel() * workspace.element_size(),
         _stream(stream)))
 

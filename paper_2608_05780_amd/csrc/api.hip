@@ -146,7 +146,8 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
 }
 
 struct WsLayout {
-  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, total;
+  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, cpart,
+      total;
   size_t segv, lse2v, intra_part, cue_total;   // frame cues, after `total`
 };
 
@@ -172,8 +173,10 @@ WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
     w.kbar = take((size_t)P.hkv * nb * d * 4);
     w.rbits = take((size_t)P.hq * nb * P.hist_words * 64 * 4);
     w.ubits = take((size_t)P.hq * nb * P.hist_words * 4);
+    w.cpart = take(evisel::coarse_part_floats((int)P.tiles.size(), P.hq,
+                                              P.hist_words) * 4);
   } else {
-    w.kbar = w.rbits = w.ubits = 0;
+    w.kbar = w.rbits = w.ubits = w.cpart = 0;
   }
   w.total = off;
   const int fpt = P.layout.Nv >= 1 && 64 % P.layout.Nv == 0
@@ -201,6 +204,7 @@ evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp,
   w.kbar = topp ? (void*)(wb + wl.kbar) : nullptr;
   w.rbits = topp ? (uint32_t*)(wb + wl.rbits) : nullptr;
   w.ubits = topp ? (uint32_t*)(wb + wl.ubits) : nullptr;
+  w.cpart = topp ? (float*)(wb + wl.cpart) : nullptr;
   w.segv = cues ? (float*)(wb + wl.segv) : nullptr;
   w.lse2v = cues ? (float*)(wb + wl.lse2v) : nullptr;
   w.intra_part = cues ? (float*)(wb + wl.intra_part) : nullptr;
@@ -480,6 +484,34 @@ evisel_status evisel_mask_export_pairs(const evisel_mask* m, int32_t* a,
     if (a) a[i] = pr[i].a;
     if (b) b[i] = pr[i].b;
   }
+  return EVISEL_OK;
+}
+
+evisel_status evisel_coarse_evidence(const evisel_mask* m, const void* q,
+                                     const void* k, int32_t d,
+                                     evisel_dtype dtype, float softmax_scale,
+                                     float* evidence, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  const evisel::Plan& P = m->plan;
+  if (!(P.rule.tau > 0.f))
+    return fail(EVISEL_ERR_INVALID_ARG,
+                "the coarse map needs a top-p mask (tau_p > 0)");
+  if (!evidence || ((uintptr_t)evidence & 3))
+    return fail(EVISEL_ERR_INVALID_ARG, "null or misaligned evidence");
+  const WsLayout wl = ws_layout(P, d);
+  st = check_qk(P, q, k, d, dtype, softmax_scale, workspace, workspace_bytes,
+                wl);
+  if (st != EVISEL_OK) return st;
+  const evisel::Workspace w = carve(wl, workspace, true);
+  const evisel::SelCall c = sel_call(q, k, d, dtype, softmax_scale,
+                                     P.rule.tau, w.rbits, w.ubits);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = evisel::launch_select(m->dp, w, c, s);
+  if (e != hipSuccess) return hip_fail(e, "retention launch");
+  e = evisel::launch_coarse(m->dp, w, c, w.cpart, evidence, s);
+  if (e != hipSuccess) return hip_fail(e, "coarse evidence launch");
   return EVISEL_OK;
 }
 

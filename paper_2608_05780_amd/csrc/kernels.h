@@ -45,6 +45,7 @@ struct Workspace {
   void* kbar;              // bf16: hi [hkv][nb][d] then lo; fp32: [hkv][nb][d]
   uint32_t* rbits;         // [hq][nb][W][64] retained history per row
   uint32_t* ubits;         // [hq][nb][W]     union over the block's rows
+  float* cpart;            // coarse evidence per-block partial sums
   // frame cues (null unless requested)
   float* segv;             // [hq][nnz][64 / N_v][64] log2 partial mass of a
                            // visual row on each frame of a computed key tile
@@ -84,6 +85,13 @@ hipError_t launch_attention(const DevPlan& p, const Workspace& w,
 size_t select_lds_need(int nh_max, int W);
 hipError_t launch_select(const DevPlan& p, const Workspace& w,
                          const SelCall& c, hipStream_t s);
+// Coarse query-frame evidence of one layer (top-p masks; the retention
+// bits must already be in w.rbits): out [hq][T]. cpart holds
+// coarse_part_floats() floats of per-block partial sums.
+size_t coarse_part_floats(int n_tiles, int hq, int W);
+hipError_t launch_coarse(const DevPlan& p, const Workspace& w,
+                         const SelCall& c, float* cpart, float* out,
+                         hipStream_t s);
 // Sets the per-(row, frame) partial masses to -inf (top-p: key tiles no row
 // of a work item retained are skipped and leave no partial).
 hipError_t launch_seg_fill(const DevPlan& p, const Workspace& w,

@@ -40,6 +40,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSelThreads = 256;
+constexpr int kTile64 = 64;
 constexpr size_t kSelLdsTwoPerCu = 80 * 1024;
 constexpr size_t kSelLdsMax = 160 * 1024;
 
@@ -353,6 +354,88 @@ __device__ __forceinline__ void retain_row_lds(float* my, int L, int cnt,
   }
 }
 
+// Affinities g = q . kbar * scale * log2(e) of rows r0 + rl (rl < rows) of
+// query block qb, head h, against its history blocks j < nh (global block
+// first + j), written to ev[rl * stride + j]. A wave takes the 32-row group
+// rg and every wpg-th 32-block tile from ph: S^T = Kbar Q^T on bf16 MFMA
+// with kbar = hi + lo accumulated into one fp32 tile (fp32: 32x32x2 MFMA).
+template <bool F32, int D>
+__device__ __forceinline__ void affinity_tiles(
+    const DevPlan& pl, const void* kbar, const void* q, float scale_log2,
+    const BlockDesc& qb, int h, int kvh, int first, int nh, int r0, int rows,
+    int rg, int ph, int wpg, float* ev, int stride, int lane) {
+  const int l32 = lane & 31, g = lane >> 5;
+  const int ntile = (nh + 31) / 32;
+  const int rl = rg * 32 + l32;
+  const bool rv = rl < rows && r0 + rl < qb.len;
+  const size_t qoff = ((size_t)(qb.start + r0 + rl) * pl.hq + h) * D;
+  if (!F32) {
+    bf16x8 qf[D / 16];
+    const __bf16* qs = (const __bf16*)q + qoff + 8 * g;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      bf16x8 z = {};
+      qf[kk] = rv ? *(const bf16x8*)(qs + 16 * kk) : z;
+    }
+    const __bf16* kh0 =
+        (const __bf16*)kbar + ((size_t)kvh * pl.nb + first) * D + 8 * g;
+    const size_t lo_off = (size_t)pl.hkv * pl.nb * D;
+    for (int t = ph; t < ntile; t += wpg) {
+      const int jb = min(32 * t + l32, nh - 1);
+      const __bf16* kh = kh0 + (size_t)jb * D;
+      f32x16 acc = {};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 ah = *(const bf16x8*)(kh + 16 * kk);
+        const bf16x8 al = *(const bf16x8*)(kh + lo_off + 16 * kk);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, qf[kk], acc, 0, 0,
+                                                      0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qf[kk], acc, 0, 0,
+                                                      0);
+      }
+      if (rv) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+          if (j < nh) ev[rl * stride + j] = acc[r] * scale_log2;
+        }
+      }
+    }
+  } else {
+    float qf[D / 2];
+    const float* qs = (const float*)q + qoff + g * (D / 2);
+#pragma unroll
+    for (int u = 0; u < D / 8; ++u) {
+      f32x4 z = {};
+      const f32x4 v = rv ? *(const f32x4*)(qs + 4 * u) : z;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) qf[4 * u + e] = v[e];
+    }
+    const float* k0 =
+        (const float*)kbar + ((size_t)kvh * pl.nb + first) * D + g * (D / 2);
+    for (int t = ph; t < ntile; t += wpg) {
+      const int jb = min(32 * t + l32, nh - 1);
+      const float* kr = k0 + (size_t)jb * D;
+      f32x16 acc = {};
+#pragma unroll
+      for (int u = 0; u < D / 8; ++u) {
+        const f32x4 a = *(const f32x4*)(kr + 4 * u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], qf[4 * u + e], acc,
+                                                     0, 0, 0);
+      }
+      if (rv) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+          if (j < nh) ev[rl * stride + j] = acc[r] * scale_log2;
+        }
+      }
+    }
+  }
+}
+
 template <bool F32, int D, int TPR>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const DevPlan pl, const Workspace ws, const SelCall sc) {
@@ -381,82 +464,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 
   const int kvh = h / (pl.hq / pl.hkv);
   const int first = qbid - nh;                    // global id of local 0
-  const int l32 = lane & 31, g = lane >> 5;
   const int rg = wave % NRG, ph = wave / NRG;
-  const int ntile = (nh + 31) / 32;
 
   for (int r0 = 0; r0 < qb.len; r0 += RPW) {
     // ---- affinities of rows r0 .. r0 + RPW - 1 against the history ----
-    {
-      const int rl = rg * 32 + l32;
-      const bool rv = rl < RPW && r0 + rl < qb.len;
-      const size_t qoff = ((size_t)(qb.start + r0 + rl) * pl.hq + h) * D;
-      if (!F32) {
-        bf16x8 qf[D / 16];
-        const __bf16* qs = (const __bf16*)sc.q + qoff + 8 * g;
-#pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          bf16x8 z = {};
-          qf[kk] = rv ? *(const bf16x8*)(qs + 16 * kk) : z;
-        }
-        const __bf16* kh0 = (const __bf16*)ws.kbar +
-                            ((size_t)kvh * pl.nb + first) * D + 8 * g;
-        const size_t lo_off = (size_t)pl.hkv * pl.nb * D;
-        for (int t = ph; t < ntile; t += WPG) {
-          const int jb = min(32 * t + l32, nh - 1);
-          const __bf16* kh = kh0 + (size_t)jb * D;
-          f32x16 acc = {};
-#pragma unroll
-          for (int kk = 0; kk < D / 16; ++kk) {
-            const bf16x8 ah = *(const bf16x8*)(kh + 16 * kk);
-            const bf16x8 al = *(const bf16x8*)(kh + lo_off + 16 * kk);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, qf[kk], acc, 0,
-                                                          0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qf[kk], acc, 0,
-                                                          0, 0);
-          }
-          if (rv) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-              if (j < nh) ev[rl * stride + j] = acc[r] * sc.scale_log2;
-            }
-          }
-        }
-      } else {
-        float qf[D / 2];
-        const float* qs = (const float*)sc.q + qoff + g * (D / 2);
-#pragma unroll
-        for (int u = 0; u < D / 8; ++u) {
-          f32x4 z = {};
-          const f32x4 v = rv ? *(const f32x4*)(qs + 4 * u) : z;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) qf[4 * u + e] = v[e];
-        }
-        const float* k0 = (const float*)ws.kbar +
-                          ((size_t)kvh * pl.nb + first) * D + g * (D / 2);
-        for (int t = ph; t < ntile; t += WPG) {
-          const int jb = min(32 * t + l32, nh - 1);
-          const float* kr = k0 + (size_t)jb * D;
-          f32x16 acc = {};
-#pragma unroll
-          for (int u = 0; u < D / 8; ++u) {
-            const f32x4 a = *(const f32x4*)(kr + 4 * u);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], qf[4 * u + e],
-                                                         acc, 0, 0, 0);
-          }
-          if (rv) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-              if (j < nh) ev[rl * stride + j] = acc[r] * sc.scale_log2;
-            }
-          }
-        }
-      }
-    }
+    affinity_tiles<F32, D>(pl, ws.kbar, sc.q, sc.scale_log2, qb, h, kvh, first,
+                           nh, r0, RPW, rg, ph, WPG, ev, stride, lane);
     __syncthreads();
 
     // ---- retention of each row (TPR lanes per row) ----
@@ -487,6 +500,206 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     for (int r = 0; r < 64; ++r) u |= wb[r * W + w];
     ub[w] = u;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Coarse query-frame evidence (appendix, coarse-map equation): for a query
+// token i, the tokens of each retained history block j share the block
+// affinity g_ij, the tokens of E_i (the video's system prefix and the causal
+// prefix of i's own block) keep their exact logits, and the row is
+// normalised. A retained block therefore carries the mass
+// len_j 2^(g_ij - M) / Z with Z = sum_{m in E_i} 2^(s_im - M) +
+// sum_{j in S_i} len_j 2^(g_ij - M) (log2 units). coarse_kernel takes one
+// query-token block, one head and one pass of 16 rows; the 16 lanes of a
+// row walk its history share. The per-block masses of the pass's rows are
+// summed in row order into cpart; coarse_reduce_kernel adds a video's
+// blocks and passes in order and spreads each block's mass evenly over its
+// frames (frames never cross blocks).
+constexpr int kCoarseTPR = 16;
+constexpr int kCoarseRows = kSelThreads / kCoarseTPR;   // rows per pass
+constexpr int kCoarsePasses = kTile64 / kCoarseRows;
+
+__device__ __forceinline__ float pair_max_(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                            __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum_(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                            __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Log2 max and sum of row r0 + l32's exact logits over the E_i tiles e =
+// ph, ph + 4, ... (system-prefix blocks, then the row's own block).
+template <bool F32, int D>
+__device__ __forceinline__ void exact_part(
+    const DevPlan& pl, const SelCall& sc, const BlockDesc& qb, int qbid,
+    int h, int kvh, int sys0, int nsys, int r0, int ph, int lane, float& mw,
+    float& lw) {
+  const int l32 = lane & 31, g = lane >> 5;
+  const bool rv = l32 < kCoarseRows && r0 + l32 < qb.len;
+  const int qtok = qb.start + r0 + l32;
+  const size_t qoff = ((size_t)(rv ? qtok : qb.start) * pl.hq + h) * D;
+  mw = -__builtin_inff();
+  lw = 0.f;
+  for (int e = ph; e <= nsys; e += 4) {
+    const int kbid = e < nsys ? sys0 + e : qbid;
+    const BlockDesc kb = pl.blocks[kbid];
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int key = min(32 * c + l32, kb.len - 1);
+      const size_t koff = ((size_t)(kb.start + key) * pl.hkv + kvh) * D;
+      if (!F32) {
+        const __bf16* ks = (const __bf16*)sc.k + koff + 8 * g;
+        const __bf16* qs = (const __bf16*)sc.q + qoff + 8 * g;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+          s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(ks + 16 * kk), *(const bf16x8*)(qs + 16 * kk),
+              s[c], 0, 0, 0);
+      } else {
+        const float* ks = (const float*)sc.k + koff + g * (D / 2);
+        const float* qs = (const float*)sc.q + qoff + g * (D / 2);
+#pragma unroll
+        for (int u = 0; u < D / 2; ++u)
+          s[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(ks[u], qs[u], s[c], 0, 0,
+                                                      0);
+      }
+    }
+    float mt = -__builtin_inff();
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
+        const bool ok = rv && key < kb.len && kb.start + key <= qtok;
+        s[c][r] = ok ? s[c][r] * sc.scale_log2 : -__builtin_inff();
+        mt = fmaxf(mt, s[c][r]);
+      }
+    mt = pair_max_(mt);
+    const float mn = fmaxf(mw, mt);
+    if (mn == -__builtin_inff()) continue;
+    float t = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t += __builtin_amdgcn_exp2f(s[c][r] - mn);
+    t = pair_sum_(t);
+    lw = (mw == -__builtin_inff() ? 0.f : lw * __builtin_amdgcn_exp2f(mw - mn))
+         + t;
+    mw = mn;
+  }
+}
+
+template <bool F32, int D>
+__global__ __launch_bounds__(kSelThreads) void coarse_kernel(
+    const DevPlan pl, const Workspace ws, const SelCall sc,
+    float* __restrict__ cpart) {
+  constexpr int TPR = kCoarseTPR, RPW = kCoarseRows;
+  extern __shared__ __attribute__((aligned(16))) float dyn[];
+  const int tile = blockIdx.x, h = blockIdx.y, pass = blockIdx.z;
+  const TextTile tt = pl.tiles[tile];
+  const int qbid = tt.qblock;
+  const BlockDesc qb = pl.blocks[qbid];
+  const int r0 = pass * RPW;
+  const int nh = pl.blk_local[qbid];
+  const int Wb = pl.W * 32;
+  float* const dst = cpart + (((size_t)tile * kCoarsePasses + pass) * pl.hq +
+                              h) * Wb;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if (r0 >= qb.len || nh <= 0) {
+    for (int j = tid; j < Wb; j += kSelThreads) dst[j] = 0.f;
+    return;
+  }
+  const int L = sel_per_thread(nh, TPR), stride = sel_stride(nh, TPR);
+  float* const ev = dyn;                      // [RPW][stride]
+  float* const emx = dyn + RPW * stride;      // [4 waves][32 rows]
+  float* const esm = emx + 4 * 32;
+  const int kvh = h / (pl.hq / pl.hkv);
+  const int first = qbid - nh;                // first visual block
+  const SeqDesc sq = pl.seqs[tt.seq];
+  const int nsys = (sq.vis0 - sq.tok0 + kTile64 - 1) / kTile64;
+  affinity_tiles<F32, D>(pl, ws.kbar, sc.q, sc.scale_log2, qb, h, kvh, first,
+                         nh, r0, RPW, 0, wave, 4, ev, stride, lane);
+  float mw, lw;
+  exact_part<F32, D>(pl, sc, qb, qbid, h, kvh, first - nsys, nsys, r0, wave,
+                     lane, mw, lw);
+  if ((lane >> 5) == 0) {
+    emx[wave * 32 + lane] = mw;
+    esm[wave * 32 + lane] = lw;
+  }
+  __syncthreads();
+  const int rr = tid / TPR, part = tid % TPR;
+  const int row = r0 + rr;
+  if (row < qb.len) {                         // uniform over the group
+    float mE = -__builtin_inff(), lE = 0.f;   // waves' parts, in order
+    for (int w = 0; w < 4; ++w) {
+      const float m = emx[w * 32 + rr], l = esm[w * 32 + rr];
+      if (m == -__builtin_inff()) continue;
+      const float mn = fmaxf(mE, m);
+      lE = (mE == -__builtin_inff() ? 0.f
+                                    : lE * __builtin_amdgcn_exp2f(mE - mn)) +
+           l * __builtin_amdgcn_exp2f(m - mn);
+      mE = mn;
+    }
+    const uint32_t* rbw =
+        ws.rbits + ((size_t)h * pl.nb + qbid) * pl.W * 64 + row;
+    const int j0 = part * L;
+    const int cnt = max(0, min(L, nh - j0));
+    float* const my = ev + rr * stride + j0;
+    float mx = -__builtin_inff();
+    for (int i = 0; i < cnt; ++i) {
+      const int j = j0 + i;
+      const bool kept = (rbw[(size_t)(j >> 5) * 64] >> (j & 31)) & 1u;
+      const float a = kept ? my[i] + __builtin_amdgcn_logf(
+                                         (float)pl.blocks[first + j].len)
+                           : -__builtin_inff();
+      my[i] = a;
+      mx = fmaxf(mx, a);
+    }
+    const float M = fmaxf(grp_max<TPR>(mx), mE);
+    float z = 0.f;
+    for (int i = 0; i < cnt; ++i) {
+      const float w = __builtin_amdgcn_exp2f(my[i] - M);
+      my[i] = w;
+      z += w;
+    }
+    z = grp_sum<TPR>(z) + lE * __builtin_amdgcn_exp2f(mE - M);
+    const float inv = 1.f / z;
+    for (int i = 0; i < cnt; ++i) my[i] *= inv;
+  }
+  __syncthreads();
+  for (int j = tid; j < Wb; j += kSelThreads) {
+    float t = 0.f;
+    if (j < nh)
+      for (int r = 0; r < RPW && r0 + r < qb.len; ++r) t += ev[r * stride + j];
+    dst[j] = t;
+  }
+}
+
+// out[h][f] = sum over the video's query blocks and passes (in order) of
+// the mass of f's block, times the share of the block's tokens in frame f.
+__global__ __launch_bounds__(256) void coarse_reduce_kernel(
+    const DevPlan pl, const float* __restrict__ cpart,
+    float* __restrict__ out) {
+  const int f = blockIdx.x * 256 + threadIdx.x, h = blockIdx.y;
+  if (f >= pl.T) return;
+  const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
+  const int Wb = pl.W * 32;
+  float t = 0.f;
+  if (sq.n_tiles > 0) {
+    const int qb0 = pl.tiles[sq.tile0].qblock;
+    const int first = qb0 - pl.blk_local[qb0];
+    const int j = (int)(((int64_t)(f - sq.frame0) * pl.Nv) / kTile64);
+    for (int ti = sq.tile0; ti < sq.tile0 + sq.n_tiles; ++ti)
+      for (int ps = 0; ps < kCoarsePasses; ++ps)
+        t += cpart[(((size_t)ti * kCoarsePasses + ps) * pl.hq + h) * Wb + j];
+    t *= (float)pl.Nv / (float)pl.blocks[first + j].len;
+  }
+  out[(size_t)h * pl.T + f] = t;
 }
 
 __global__ void seg_fill_kernel(float* __restrict__ p, size_t n) {
@@ -564,6 +777,41 @@ hipError_t launch_select(const DevPlan& p, const Workspace& w,
                      : launch_sel_d<true, 128>(p, w, c, nh_max, s);
   return c.d == 64 ? launch_sel_d<false, 64>(p, w, c, nh_max, s)
                    : launch_sel_d<false, 128>(p, w, c, nh_max, s);
+}
+
+size_t coarse_part_floats(int n_tiles, int hq, int W) {
+  return (size_t)n_tiles * kCoarsePasses * hq * W * 32;
+}
+
+hipError_t launch_coarse(const DevPlan& p, const Workspace& w,
+                         const SelCall& c, float* cpart, float* out,
+                         hipStream_t s) {
+  if (p.n_tiles > 0) {
+    const int nh_max = std::max(p.hmax, 1);
+    const size_t lds = (size_t)kCoarseRows *
+                           sel_stride(nh_max, kCoarseTPR) * 4 + 2 * 4 * 32 * 4;
+    dim3 grid(p.n_tiles, p.hq, kCoarsePasses), block(kSelThreads);
+    auto go = [&](auto fn) -> hipError_t {
+      if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute(
+            (const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+            (int)lds);
+        if (e != hipSuccess) return e;
+      }
+      fn<<<grid, block, lds, s>>>(p, w, c, cpart);
+      return hipGetLastError();
+    };
+    hipError_t e;
+    if (c.fp32)
+      e = c.d == 64 ? go(coarse_kernel<true, 64>) : go(coarse_kernel<true, 128>);
+    else
+      e = c.d == 64 ? go(coarse_kernel<false, 64>)
+                    : go(coarse_kernel<false, 128>);
+    if (e != hipSuccess) return e;
+  }
+  coarse_reduce_kernel<<<dim3((p.T + 255) / 256, p.hq), dim3(256), 0, s>>>(
+      p, cpart, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_seg_fill(const DevPlan& p, const Workspace& w,
