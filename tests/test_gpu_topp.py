@@ -41,9 +41,10 @@ def _layout(w, seed=0):
     return Layout(ns, nf, nt, w.tokens_per_frame)
 
 
-def _gpu_bits(ev, mask, w, layer, seed=0):
+def _gpu_bits(ev, mask, w, layer, seed=0, inputs=None):
     import torch
-    q, k, _ = to_device(wl.gen_layer(w, layer, seed), w, torch)
+    inputs = inputs if inputs is not None else wl.gen_layer(w, layer, seed)
+    q, k, _ = to_device(inputs, w, torch)
     st = mask.stats
     nb, W = st["n_blocks"], st["hist_words"]
     rb = torch.full((w.hq, nb, W, 64), -1, dtype=torch.int32, device="cuda")
@@ -129,14 +130,15 @@ def _run_case(w, rows_budget=None, seed=0, layers=None):
     blk = topp.Blocks(lay, w.block)
     layers = layers if layers is not None else list(range(w.n_layers))
     keeps = {}
-    res = run_gpu(ev, w, layers, seed)
+    inputs = {l: wl.gen_layer(w, l, seed) for l in layers}
+    res = run_gpu(ev, w, layers, seed, layer_inputs=lambda l: inputs[l])
     for j, l in enumerate(layers):
-        q, k, v = wl.gen_layer(w, l, seed).as_f64()
+        q, k, v = inputs[l].as_f64()
         rows = (np.arange(lay.S) if rows_budget is None else
                 sample_rows(lay, rows_budget, seed + 17 * l))
         ref = topp.run_layer(q, k, v, lay, w.block, w.tau_p,
                              w.softmax_scale, rows)
-        rb, ub = _gpu_bits(ev, res.mask, w, l, seed)
+        rb, ub = _gpu_bits(ev, res.mask, w, l, seed, inputs=inputs[l])
         mc = ref["keep"].shape[2]
         kg = _keep_of_rows(ev, rb, res.mask, blk, rows, mc)
         match, _ = _classify(q, k, lay, blk, rows, ref["keep"], kg,
@@ -307,6 +309,20 @@ def test_topp_config2_layer():
     w = wl.get(2, tau_p=TAU)
     say("case config-2 top-p")
     _run_case(w, rows_budget=512)
+
+
+def test_topp_config4_long_video():
+    # 1,026 selectable blocks: 33 history words, LDS-streaming retention
+    w = wl.get(4, tau_p=TAU)
+    say("case config-4 top-p, layer 0")
+    _run_case(w, rows_budget=256, layers=[0])
+
+
+def test_topp_config5_ragged_batch():
+    # eight videos of 64-512 frames x 32 tokens, two frames per block
+    w = wl.get(5, tau_p=TAU)
+    say("case config-5 top-p, layer 0")
+    _run_case(w, rows_budget=512, layers=[0])
 
 
 def test_topp_config3_two_layers():
