@@ -11,7 +11,8 @@
 //
 // Key/value tiles go straight from global memory to LDS (16-byte
 // global_load_lds per lane, no staging registers), double-buffered: tile j+1
-// is in flight while tile j is computed, one barrier per tile. Rows are
+// is in flight while tile j is computed, one barrier per tile. The K operand
+// reads of a tile run eight ahead of the MFMAs that consume them. Rows are
 // XOR-swizzled in 16-byte chunks so the MFMA operand reads below are free of
 // LDS bank conflicts.
 //
@@ -101,6 +102,21 @@ __device__ __forceinline__ int swz(int row) {
   return 0;
 }
 
+// One 16-byte-per-lane global -> LDS load: lane l's 16 bytes from
+// gbase + voff land at LDS byte address lds + 16 l. Issued as inline
+// assembly so that the compiler does not treat later LDS reads as possibly
+// racing with it (it would otherwise wait for every outstanding load,
+// including the next tile's, before the transposed V reads); every caller
+// waits for vmcnt(0) and a barrier before reading the destination.
+__device__ __forceinline__ void lds_dma16(uint32_t lds, const char* gbase,
+                                          uint32_t voff) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+      :
+      : "s"(lds), "v"(voff), "s"(gbase)
+      : "memory", "m0");
+}
+
 // Loads of one 64-key tile of a [S][H][D] tensor into LDS: every thread
 // fetches N = 64*RC/256 chunks of 16 bytes and a wavefront's load fills 64
 // consecutive 16-byte LDS slots. The (row, chunk) a lane fetches is fixed,
@@ -133,21 +149,18 @@ struct TileLoader {
     const char* base =
         (const char*)src + ((size_t)kstart * rowbytes + (size_t)kvh * D *
                                                             sizeof(T));
+    const uint32_t lds0 =
+        (uint32_t)(uintptr_t)buf + (uint32_t)(wave * N * 1024);
     if (klen == kTile) {
 #pragma unroll
-      for (int i = 0; i < N; ++i)
-        __builtin_amdgcn_global_load_lds(
-            (const void*)(base + off[i]),
-            (EV_LDS void*)(buf + (wave * N + i) * 1024), 16, 0, 0);
+      for (int i = 0; i < N; ++i) lds_dma16(lds0 + i * 1024, base, off[i]);
     } else {
 #pragma unroll
       for (int i = 0; i < N; ++i) {
         const int r = row0 + i * RSTEP;
         const uint32_t over =
             r >= klen ? (uint32_t)(r - (klen - 1)) * rowbytes : 0u;
-        __builtin_amdgcn_global_load_lds(
-            (const void*)(base + (off[i] - over)),
-            (EV_LDS void*)(buf + (wave * N + i) * 1024), 16, 0, 0);
+        lds_dma16(lds0 + i * 1024, base, off[i] - over);
       }
     }
   }
@@ -177,17 +190,29 @@ struct Bf16Path {
   // logical chunk 2kk + g of K row key.
   __device__ static void qk(f32x16 (&s)[2], const EV_LDS char* kt,
                             const QFrag& qf, int l32, int g) {
+    bf16x8 kf[D / 16][2];
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
+    for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const int key = 32 * c + l32;
         const int ch = (2 * kk + g) ^ swz<kSwzK, RC>(key);
-        const bf16x8 kf = *(const EV_LDS bf16x8*)(kt + (key * RC + ch) * 16);
-        s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf.x[kk], s[c], 0,
-                                                        0, 0);
+        kf[kk][c] = *(const EV_LDS bf16x8*)(kt + (key * RC + ch) * 16);
       }
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk][c], qf.x[kk],
+                                                        s[c], 0, 0, 0);
+    // eight operand reads ahead, then two MFMAs per two further reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < D / 16 - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
   }
 
   // O^T[d][q] += V^T[d][key] P^T[key][q]. The B operand of k-step (c, s)
@@ -406,13 +431,14 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       }
     }
     if (cur.len < kTile || cur.start + cur.len - 1 > qb.start) {
+      // key kl = 32c + 8(r/4) + 4g + r%4 is masked when kl >= len or
+      // start + kl > qpos, i.e. when its lane-free part exceeds x
+      const int x = min(qpos - cur.start, cur.len - 1) - 4 * g;
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (kl >= cur.len || cur.start + kl > qpos) s[c][r] = neg_inf();
-        }
+        for (int r = 0; r < 16; ++r)
+          if (32 * c + 8 * (r >> 2) + (r & 3) > x) s[c][r] = neg_inf();
     }
     float mx = neg_inf();
 #pragma unroll

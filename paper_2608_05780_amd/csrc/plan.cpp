@@ -11,6 +11,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <map>
 #include <numeric>
 
 namespace evisel {
@@ -19,6 +20,7 @@ namespace {
 struct Item {
   WorkItem w;
   int64_t cost;
+  int64_t group = 0;   // query-token items: (video, kv head, chunk)
 };
 
 }  // namespace
@@ -215,7 +217,8 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
             const int32_t e = rb + (int32_t)((int64_t)(c + 1) * len / nch);
             WorkItem w{b, h0, nh, a, e, tt.slot0 + h0 * nch + c, (int32_t)n,
                        nch};
-            txt_items.push_back({w, e - a + 1});
+            txt_items.push_back(
+                {w, e - a + 1, ((int64_t)n * hkv + g) * 65536 + c});
           }
         }
       P.n_slots += (int64_t)hq * nch;
@@ -242,15 +245,29 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   // Longest-first over the XCD queues: split query-token items go first, by
   // LPT; the remaining items keep their locality order and are cut into
   // contiguous runs that level the queues.
-  std::stable_sort(txt_items.begin(), txt_items.end(),
-                   [](const Item& a, const Item& b) { return a.cost > b.cost; });
+  // Query-token items that read the same key range (same video, kv head
+  // and chunk) go to one XCD together, so that its L2 fetches the range
+  // once; the groups are balanced longest-first over the XCDs.
+  std::map<int64_t, std::vector<Item>> groups;
+  for (const Item& it : txt_items) groups[it.group].push_back(it);
+  std::vector<std::pair<int64_t, int64_t>> gcost;   // (cost, key)
+  for (auto& kv : groups) {
+    int64_t c = 0;
+    for (const Item& it : kv.second) c += it.cost;
+    gcost.push_back({c, kv.first});
+  }
+  std::stable_sort(gcost.begin(), gcost.end(),
+                   [](const std::pair<int64_t, int64_t>& a,
+                      const std::pair<int64_t, int64_t>& b) {
+                     return a.first > b.first;
+                   });
   std::vector<std::vector<WorkItem>> q(kXcds);
   std::vector<int64_t> load(kXcds, 0);
-  for (const Item& it : txt_items) {
+  for (const auto& gc : gcost) {
     const int x = (int)(std::min_element(load.begin(), load.end()) -
                         load.begin());
-    q[x].push_back(it.w);
-    load[x] += it.cost;
+    for (const Item& it : groups[gc.second]) q[x].push_back(it.w);
+    load[x] += gc.first;
   }
   int64_t rest = 0;
   for (const Item& it : other_items) rest += it.cost;
