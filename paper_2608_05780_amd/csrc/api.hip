@@ -94,6 +94,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   const evisel::Plan& P = m->plan;
   std::vector<char> buf;
   const size_t o_blk = put(buf, P.blocks), o_col = put(buf, P.col),
+               o_cd = put(buf, P.col_desc),
                o_it = put(buf, P.items), o_seq = put(buf, P.seqs),
                o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq),
                o_bl = put(buf, P.blk_local), o_fp = put(buf, P.pairs),
@@ -114,6 +115,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   evisel::DevPlan& dp = m->dp;
   dp.blocks = (const evisel::BlockDesc*)(d + o_blk);
   dp.col = (const int32_t*)(d + o_col);
+  dp.col_desc = (const evisel::BlockDesc*)(d + o_cd);
   dp.items = (const evisel::WorkItem*)(d + o_it);
   dp.seqs = (const evisel::SeqDesc*)(d + o_seq);
   dp.tiles = (const evisel::TextTile*)(d + o_tt);

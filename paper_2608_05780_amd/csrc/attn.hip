@@ -40,6 +40,13 @@
 //                      transpose read: within 16 lanes, lane i receives
 //                      element i % 4 of the rows addressed by lanes i/4 + 4k).
 //
+// bf16 Q and O pass through LDS in the K-tile layout: the item's Q rows are
+// read as whole 256-byte rows into the second buffer pair (free until the
+// first loop iteration refills it after a barrier), and the normalised O
+// rows are written back the same way after the last tile. Read or written
+// straight from the MFMA layout, every such instruction touches 32 rows
+// 7 KB apart, 16-32 bytes each.
+//
 // Visual and system rows finish in the kernel (O, LSE). Query-token rows are
 // split into chunks of key blocks (longest-first balance across the chip);
 // each chunk leaves an unnormalised partial (acc, m_ref, row sum, non-visual
@@ -226,39 +233,139 @@ struct Bf16Path {
                             const f32x16 (&p)[2], int lane) {
     const int j = lane & 15, q16 = lane >> 4, g = lane >> 5;
     const int sw = swz<kSwzV, RC>(j >> 2);   // row % 4 == j / 4 below
+    constexpr int NMT = D / 32;
+    bf16x8 va[4][NMT];
+    bf16x8 pb[4];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int cs = 0; cs < 4; ++cs) {
+      const int c = cs >> 1, s = cs & 1;
+      const f32x8 pf = s == 0 ? __builtin_shufflevector(p[c], p[c], 0, 1, 2, 3,
+                                                        4, 5, 6, 7)
+                              : __builtin_shufflevector(p[c], p[c], 8, 9, 10,
+                                                        11, 12, 13, 14, 15);
+      pb[cs] = __builtin_convertvector(pf, bf16x8);
+      const int row = 32 * c + 16 * s + 4 * g + (j >> 2);
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const f32x8 pf = s == 0 ? __builtin_shufflevector(p[c], p[c], 0, 1, 2,
-                                                          3, 4, 5, 6, 7)
-                                : __builtin_shufflevector(p[c], p[c], 8, 9, 10,
-                                                          11, 12, 13, 14, 15);
-        const bf16x8 pb = __builtin_convertvector(pf, bf16x8);
-        const int row = 32 * c + 16 * s + 4 * g + (j >> 2);
-#pragma unroll
-        for (int mt = 0; mt < D / 32; ++mt) {
-          const int col = 32 * mt + 16 * (q16 & 1) + 4 * (j & 3);
-          const int ch = (col >> 3) ^ sw;
-          const EV_LDS char* a0 = vt + (row * RC + ch) * 16 + 8 * (j & 1);
-          const EV_LDS char* a1 = a0 + 8 * RC * 16;   // row + 8
-          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (EV_LDS i16x4*)a0);
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (EV_LDS i16x4*)a1);
-          const i16x4 lohi[2] = {lo, hi};
-          const bf16x8 va = __builtin_bit_cast(bf16x8, lohi);
-          o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[mt], 0, 0,
-                                                          0);
-        }
+      for (int mt = 0; mt < NMT; ++mt) {
+        const int col = 32 * mt + 16 * (q16 & 1) + 4 * (j & 3);
+        const int ch = (col >> 3) ^ sw;
+        const EV_LDS char* a0 = vt + (row * RC + ch) * 16 + 8 * (j & 1);
+        const EV_LDS char* a1 = a0 + 8 * RC * 16;   // row + 8
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (EV_LDS i16x4*)a0);
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (EV_LDS i16x4*)a1);
+        const i16x4 lohi[2] = {lo, hi};
+        va[cs][mt] = __builtin_bit_cast(bf16x8, lohi);
       }
     }
+#pragma unroll
+    for (int cs = 0; cs < 4; ++cs)
+#pragma unroll
+      for (int mt = 0; mt < NMT; ++mt)
+        o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[cs][mt], pb[cs],
+                                                        o[mt], 0, 0, 0);
+    // eight transpose reads (four operands) ahead, then one MFMA per two
+    // further reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 4 * NMT - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   }
 
   __device__ static void store_o(void* out, int qpos, int h, int hq, int d0,
                                  f32x4 v) {
     bf16x4 b = __builtin_convertvector(v, bf16x4);
     *(bf16x4*)((__bf16*)out + ((size_t)qpos * hq + h) * D + d0) = b;
+  }
+  // Q and O move through LDS in the K-tile layout (rows of RC swizzled
+  // 16-byte chunks), so that every global access is a whole row: 16 lanes
+  // cover one row of one head.
+  static constexpr bool kStaged = true;
+  static constexpr int kPer = kTile * RC / kThreads;   // chunks per thread
+
+  // Staged Q in two halves, so that its global loads share a round trip
+  // with the first tile's: stage_q_load reads rows [start, start+len) of
+  // heads h0 and, when nh is 2, h0+1 into registers (rows past len repeat
+  // the last row), stage_q_store writes them to d0 / d1 (rows past len as
+  // zeros).
+  struct QStage {
+    bf16x8 v[2][kPer];
+  };
+  __device__ static void stage_q_load(QStage& st, const void* q, int start,
+                                      int len, int h0, int nh, int hq,
+                                      int tid) {
+    const __bf16* src = (const __bf16*)q;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      if (hh < nh) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+          const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
+          const int r = min(row, len - 1);
+          st.v[hh][i] = *(const bf16x8*)(src + ((size_t)(start + r) * hq +
+                                                h0 + hh) * D + ch * 8);
+        }
+      }
+    }
+  }
+  __device__ static void stage_q_store(const QStage& st, EV_LDS char* d0,
+                                       EV_LDS char* d1, int len, int nh,
+                                       int tid) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      if (hh < nh) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+          const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
+          const bf16x8 z = {};
+          *(EV_LDS bf16x8*)((hh ? d1 : d0) +
+                            (row * RC + (ch ^ swz<kSwzK, RC>(row))) * 16) =
+              row < len ? st.v[hh][i] : z;
+        }
+      }
+    }
+  }
+  // The B operand of row `row` from a staged Q tile (as load_q).
+  __device__ static void load_q_lds(QFrag& qf, const EV_LDS char* src,
+                                    int row, int g) {
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const int ch = (2 * kk + g) ^ swz<kSwzK, RC>(row);
+      qf.x[kk] = *(const EV_LDS bf16x8*)(src + (row * RC + ch) * 16);
+    }
+  }
+  // The lane's O^T values (times inv) of row `row` into a staged O tile:
+  // o[mt][4 r4 .. 4 r4 + 3] are d = 32 mt + 8 r4 + 4 g .. + 3.
+  __device__ static void o_to_lds(EV_LDS char* dst, const f32x16 (&o)[D / 32],
+                                  float inv, int row, int g) {
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const f32x4 v = {o[mt][4 * r4] * inv, o[mt][4 * r4 + 1] * inv,
+                         o[mt][4 * r4 + 2] * inv, o[mt][4 * r4 + 3] * inv};
+        const int ch = (4 * mt + r4) ^ swz<kSwzK, RC>(row);
+        *(EV_LDS bf16x4*)(dst + (row * RC + ch) * 16 + 8 * g) =
+            __builtin_convertvector(v, bf16x4);
+      }
+  }
+  // Rows [start, start+len) of head h from a staged O tile to out.
+  __device__ static void o_from_lds(void* out, const EV_LDS char* src,
+                                    int start, int len, int h, int hq,
+                                    int tid) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
+      if (row < len)
+        *(bf16x8*)((__bf16*)out + ((size_t)(start + row) * hq + h) * D +
+                   ch * 8) =
+            *(const EV_LDS bf16x8*)(src + (row * RC +
+                                           (ch ^ swz<kSwzK, RC>(row))) * 16);
+    }
   }
 };
 
@@ -324,6 +431,17 @@ struct F32Path {
                                  f32x4 v) {
     *(f32x4*)((float*)out + ((size_t)qpos * hq + h) * D + d0) = v;
   }
+  static constexpr bool kStaged = false;
+  struct QStage {};
+  __device__ static void stage_q_load(QStage&, const void*, int, int, int,
+                                      int, int, int) {}
+  __device__ static void stage_q_store(const QStage&, EV_LDS char*,
+                                       EV_LDS char*, int, int, int) {}
+  __device__ static void load_q_lds(QFrag&, const EV_LDS char*, int, int) {}
+  __device__ static void o_to_lds(EV_LDS char*, const f32x16 (&)[D / 32],
+                                  float, int, int) {}
+  __device__ static void o_from_lds(void*, const EV_LDS char*, int, int, int,
+                                    int, int) {}
 };
 
 // ---------------------------------------------------------------------------
@@ -335,7 +453,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   constexpr int TB = kTile * P::RC * 16;   // bytes of one tile
   constexpr int VSWZ = sizeof(T) == 2 ? kSwzV : kSwzNone;
   __shared__ __attribute__((aligned(1024))) char smem[4 * TB];
-  EV_LDS char* lds = (EV_LDS char*)smem;   // [K0 | V0 | K1 | V1]
+  EV_LDS char* lds = (EV_LDS char*)smem;   // [K0 | K1 | V0 | V1]
   // top-p: CSR positions of the item's key tiles that some row retained
   __shared__ short clist[TOPP ? kMaxItemCandidates : 1];
   __shared__ int n_kept;
@@ -360,7 +478,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const T* vg = (const T*)ac.v;
 
   typename P::QFrag qf;
-  P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
+  if constexpr (!P::kStaged) P::load_q(qf, ac.q, qpos, qvalid, h, pl.hq, g);
 
   float m_ref = neg_inf(), l_part = 0.f, nv_part = 0.f;
   f32x16 o[D / 32];
@@ -376,7 +494,53 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   EV_LDS char* const vbuf0 = lds + 2 * TB;
   auto kbuf = [&](int t) { return kbuf0 + (t & 1) * TB; };
   auto vbuf = [&](int t) { return vbuf0 + (t & 1) * TB; };
+
   const int b0 = it.kb_begin;
+
+  // Descriptors of this item's key tiles, 64 at a time: lane t holds the
+  // BlockDesc of tile 64*batch + t, and the loop reads tile j's with
+  // v_readlane. (Loading them per tile would put two dependent global round
+  // trips in front of every tile's K/V loads.)
+  // Top-p: dsc_loc is the tile's local history index, or -1 when the tile
+  // is always visible.
+  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1,
+      dsc_pos = 0;
+  auto load_batch = [&](int batch) {
+    const int t = batch * 64 + lane;
+    if (t < n) {
+      const int pos = TOPP ? (int)clist[t] : t;
+      const BlockDesc bd = pl.col_desc[b0 + pos];
+      dsc_pos = pos;
+      dsc_start = bd.start;
+      dsc_len = bd.len;
+      dsc_region = bd.region;
+      dsc_aux = bd.aux;
+      if (TOPP) {
+        const int bid = pl.col[b0 + pos];
+        const int loc = pl.blk_local[bid];
+        dsc_loc = bid == it.qblock ? -1 : loc;
+      }
+    }
+  };
+  auto desc = [&](int t) {
+    const int l = t & 63;
+    BlockDesc d;
+    d.start = __builtin_amdgcn_readlane(dsc_start, l);
+    d.len = __builtin_amdgcn_readlane(dsc_len, l);
+    d.region = __builtin_amdgcn_readlane(dsc_region, l);
+    d.aux = __builtin_amdgcn_readlane(dsc_aux, l);
+    return d;
+  };
+
+  // The item's Q rows go through the second buffer pair (K1 for the first
+  // head, V1 for the second), which the first loop iteration refills only
+  // after a barrier. Without top-p the first descriptor batch is fetched
+  // here, in the same round trip as the query block's descriptor.
+  if constexpr (!TOPP) load_batch(0);
+  typename P::QStage qst;
+  if constexpr (P::kStaged)
+    P::stage_q_load(qst, ac.q, qb.start, qb.len, it.head, it.nheads, pl.hq,
+                    tid);
 
   // Top-p: a candidate tile is kept when it is always visible (system
   // prefix, the query block itself) or some row of the item's heads
@@ -523,41 +687,6 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     P::pv(o, vt, s, lane);
   };
 
-  // Descriptors of this item's key tiles, 64 at a time: lane t holds the
-  // BlockDesc of tile 64*batch + t, and the loop reads tile j's with
-  // v_readlane. (Loading them per tile would put two dependent global round
-  // trips in front of every tile's K/V loads.)
-  // Top-p: dsc_loc is the tile's local history index, or -1 when the tile
-  // is always visible.
-  int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1,
-      dsc_pos = 0;
-  auto load_batch = [&](int batch) {
-    const int t = batch * 64 + lane;
-    if (t < n) {
-      const int pos = TOPP ? (int)clist[t] : t;
-      const int bid = pl.col[b0 + pos];
-      const BlockDesc bd = pl.blocks[bid];
-      dsc_pos = pos;
-      dsc_start = bd.start;
-      dsc_len = bd.len;
-      dsc_region = bd.region;
-      dsc_aux = bd.aux;
-      if (TOPP) {
-        const int loc = pl.blk_local[bid];
-        dsc_loc = bid == it.qblock ? -1 : loc;
-      }
-    }
-  };
-  auto desc = [&](int t) {
-    const int l = t & 63;
-    BlockDesc d;
-    d.start = __builtin_amdgcn_readlane(dsc_start, l);
-    d.len = __builtin_amdgcn_readlane(dsc_len, l);
-    d.region = __builtin_amdgcn_readlane(dsc_region, l);
-    d.aux = __builtin_amdgcn_readlane(dsc_aux, l);
-    return d;
-  };
-
   // Top-p: the row's retained-history word of a tile, fetched with the
   // tile's key/value loads.
   const uint32_t* rrow =
@@ -574,7 +703,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   };
 
   // Tile j+1 streams into the other buffer pair while tile j is computed.
-  load_batch(0);
+  if constexpr (TOPP) load_batch(0);
   BlockDesc kb = desc(0);
   int lnext = loc_of(0), pnext = pos_of(0);
   unsigned wnext = 0u;
@@ -582,6 +711,11 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
     vload.issue(vbuf(0), vg, kb.start, kb.len, kvh, wave);
     if (TOPP) wnext = row_bits(lnext);
+  }
+  if constexpr (P::kStaged) {
+    P::stage_q_store(qst, kbuf(1), vbuf(1), qb.len, it.nheads, tid);
+    __syncthreads();   // staged Q visible to every wave
+    P::load_q_lds(qf, hsub ? vbuf(1) : kbuf(1), qrow, g);
   }
   for (int j = 0; j < n; ++j) {
     const BlockDesc cur = kb;
@@ -608,20 +742,31 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       tile_post(s, cur, ts, vbuf(j), pcur);
     }
   }
+  const float l_tot = pair_sum(l_part);
+  if (P::kStaged && !is_text) {
+    // O rows through LDS (K0 for the first head, K1 for the second), then
+    // whole-row stores by every thread of the work-group
+    __syncthreads();   // every wave is done with the last tile
+    if (active) P::o_to_lds(kbuf(hsub), o, qvalid ? 1.f / l_tot : 0.f, qrow, g);
+    __syncthreads();
+    for (int hh = 0; hh < it.nheads; ++hh)
+      P::o_from_lds(ac.o, kbuf(hh), qb.start, qb.len, it.head + hh, pl.hq, tid);
+  }
   if (!active) return;
 
-  const float l_tot = pair_sum(l_part);
   if (!is_text) {
     if (qvalid) {
-      const float inv = 1.f / l_tot;
+      if constexpr (!P::kStaged) {
+        const float inv = 1.f / l_tot;
 #pragma unroll
-      for (int mt = 0; mt < D / 32; ++mt)
+        for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4 v = {o[mt][4 * r4] * inv, o[mt][4 * r4 + 1] * inv,
-                     o[mt][4 * r4 + 2] * inv, o[mt][4 * r4 + 3] * inv};
-          P::store_o(ac.o, qpos, h, pl.hq, 32 * mt + 8 * r4 + 4 * g, v);
-        }
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4 v = {o[mt][4 * r4] * inv, o[mt][4 * r4 + 1] * inv,
+                       o[mt][4 * r4 + 2] * inv, o[mt][4 * r4 + 3] * inv};
+            P::store_o(ac.o, qpos, h, pl.hq, 32 * mt + 8 * r4 + 4 * g, v);
+          }
+      }
       if (g == 0 && ac.lse)
         ac.lse[(size_t)h * pl.S + qpos] = (m_ref + log2_(l_tot)) * kLn2;
       if (g == 0 && ac.lse2v)

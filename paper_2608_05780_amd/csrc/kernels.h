@@ -10,6 +10,7 @@ namespace evisel {
 struct DevPlan {
   const BlockDesc* blocks;
   const int32_t* col;
+  const BlockDesc* col_desc;  // [nnz] descriptor of each CSR entry's block
   const WorkItem* items;
   const SeqDesc* seqs;
   const TextTile* tiles;

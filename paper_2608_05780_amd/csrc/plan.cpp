@@ -136,6 +136,8 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   for (int32_t b = 0; b < nb; ++b) P.row_ptr[b + 1] += P.row_ptr[b];
   if ((int64_t)P.row_ptr[nb] != (int64_t)P.col.size())
     return "internal error: CSR size mismatch";
+  P.col_desc.resize(P.col.size());
+  for (size_t p = 0; p < P.col.size(); ++p) P.col_desc[p] = P.blocks[P.col[p]];
 
   // ---- selectable blocks (top-p bookkeeping) -------------------------------
   P.blk_local.assign(nb, -1);

@@ -100,6 +100,7 @@ struct Plan {
   // tables
   std::vector<BlockDesc> blocks;
   std::vector<int32_t> row_ptr, col;
+  std::vector<BlockDesc> col_desc;  // [nnz] descriptor of col[p]'s block
   std::vector<WorkItem> items;      // launch order
   std::vector<SeqDesc> seqs;
   std::vector<TextTile> tiles;
