@@ -87,15 +87,21 @@ def test_workload_plans(lib, cid):
 def _check_work(m, csr, hq):
     """Every (query block, head) is covered exactly once by contiguous runs of
     its CSR row; heads of an item share a kv head; query-token items use
-    distinct slots that exactly fill [0, n_chunk_slots)."""
+    distinct slots that exactly fill [0, n_chunk_slots); the query-token
+    chunks that read the same key range (same video, kv head and chunk
+    index) are launched on one XCD (work-group i runs on XCD i mod 8)."""
     wk = ev.mask_export_work(m)
     region, rp = csr["region"], csr["row_ptr"]
     group = hq // m.stats["hkv"]
     seen, text_items = {}, []
-    for qb, h0, nh, a, e, s in zip(wk["qblock"], wk["head"], wk["nheads"],
-                                   wk["kb_begin"], wk["kb_end"], wk["slot"]):
+    xcd_of = {}
+    for idx, (qb, h0, nh, a, e, s) in enumerate(zip(
+            wk["qblock"], wk["head"], wk["nheads"], wk["kb_begin"],
+            wk["kb_end"], wk["slot"])):
         if qb < 0:
             continue
+        if region[qb] == 2:
+            xcd_of[(int(qb), int(h0), int(a))] = idx % 8
         assert rp[qb] <= a < e <= rp[qb + 1]
         assert 1 <= nh <= 4 and h0 // group == (h0 + nh - 1) // group
         for i in range(nh):
@@ -115,6 +121,14 @@ def _check_work(m, csr, hq):
         nch = len(seen[(qb, h0)])
         slots.extend(s + i * nch for i in range(nh))
     assert sorted(slots) == list(range(m.stats["n_chunk_slots"]))
+    groups = {}
+    for qb, h0, nh, s in text_items:
+        runs = sorted(seen[(qb, h0)])
+        for c, (a, e) in enumerate(runs):
+            if (qb, h0, a) in xcd_of:
+                key = (int(csr["video"][qb]), h0 // group, c)
+                groups.setdefault(key, set()).add(xcd_of[(qb, h0, a)])
+    assert all(len(x) == 1 for x in groups.values()), groups
 
 
 @pytest.mark.parametrize("ci", range(len(CASES)))
