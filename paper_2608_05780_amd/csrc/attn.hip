@@ -6,15 +6,15 @@
 // blocks (CSR). A work-group has four wavefronts: waves 0-1 take the first
 // head's rows 0-31 / 32-63, waves 2-3 the second head's. Each key/value tile
 // is staged once in LDS for both heads. Two work-groups fit a CU, so every
-// SIMD interleaves two wavefronts: one's softmax VALU work overlaps the
-// other's MFMA work.
+// SIMD interleaves two wavefronts and part of one's softmax VALU work hides
+// under the other's MFMAs.
 //
 // Key/value tiles go straight from global memory to LDS (16-byte
 // global_load_lds per lane, no staging registers), double-buffered: tile j+1
-// is in flight while tile j is computed, one barrier per tile. The K operand
-// reads of a tile run eight ahead of the MFMAs that consume them. Rows are
-// XOR-swizzled in 16-byte chunks so the MFMA operand reads below are free of
-// LDS bank conflicts.
+// is in flight while tile j is computed, one barrier per tile. The K and V
+// operand reads of a tile run eight ahead of the MFMAs that consume them.
+// Rows are XOR-swizzled in 16-byte chunks so the MFMA operand reads below are
+// free of LDS bank conflicts.
 //
 // Per key tile (64 keys):
 //   S^T = K Q^T        32x32x16 bf16 MFMA (fp32 inputs: 32x32x2 f32 MFMA);
