@@ -14,8 +14,10 @@ aggregation and top-16 frames). Inputs are resident in HBM before timing.
 
 Prints one JSON line: probe tokens/s (value), ms per step, the attention
 kernel's roofline against the bf16 MFMA peak (active-block FLOPs over the
-kernel's HIP-event time, measured over the timed region), and the fp64 CPU
-oracle's throughput on a bounded sample (whole layers, at least 10 s) as a baseline.
+kernel's HIP-event time, measured over the timed region, where only that
+kernel is bracketed by events), the other kernels' times from two further
+untimed steps, and the fp64 CPU oracle's throughput on a bounded sample
+(whole layers, at least 10 s) as a baseline.
 
 ``--tau-p P`` runs the same workload under the paper's adaptive top-p
 retention instead of the static rule: every layer first selects each row's
@@ -259,15 +261,24 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    ev.profile_begin(args.steps * L)
+    # Timed region: HIP events around the attention kernel only (each event
+    # is a dependency packet between kernels, so the others run back to
+    # back); the per-kernel breakdown comes from two further, untimed steps.
+    ev.profile_begin(args.steps * L, all_kernels=False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = ev.profile_end()
+    prof_attn = ev.profile_end()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    n_detail = 2
+    ev.profile_begin(n_detail * L, all_kernels=True)
+    for _ in range(n_detail):
+        step()
+    torch.cuda.synchronize()
+    prof = ev.profile_end()
 
     found = sorted(topk[:sum(ks)].cpu().numpy().tolist())
     planted_ok = found == sorted(core.tolist())
@@ -277,7 +288,7 @@ def main():
         flop_layer = tile_flop * pairs
     else:
         flop_layer = tile_flop * w.hq * st["n_active_pairs"]
-    attn_ms = prof["attention_ms"] / max(1, prof["calls"])
+    attn_ms = prof_attn["attention_ms"] / max(1, prof_attn["calls"])
     achieved = flop_layer / (attn_ms * 1e-3) / 1e12
     ev_ms = prof["evidence_ms"] / max(1, prof["calls"])
     ev_bytes = 4.0 * w.hq * (st["n_text_rows"] * T + st["n_text_rows"] + T)
@@ -304,7 +315,9 @@ def main():
         "roofline": {"bound": "mfma", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": measured_traffic() if args.config == 3 else None,
+                     # counters cover the static-rule kernel without cues
+                     "traffic": (measured_traffic() if args.config == 3 and
+                                 w.tau_p == 0 and not args.cues else None),
                      "kernel": "attn_kernel<Bf16Path<128>>",
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms},

@@ -255,13 +255,16 @@ evisel::SelCall sel_call(const void* q, const void* k, int32_t d,
 // Kernel timing session (evisel_profile_begin / _end).
 struct Profile {
   bool open = false;
+  bool all = true;             // every kernel, else the attention kernel only
   std::vector<hipEvent_t> ev;  // kProfEvents per timed call
   size_t used = 0;             // calls recorded
 };
 Profile g_prof;
 constexpr int kProfEvents = 6;
+constexpr int kProfAttn = 1;   // events kProfAttn, kProfAttn + 1 bracket K1
 
 void prof_record(size_t call, int k, hipStream_t s) {
+  if (!g_prof.all && k != kProfAttn && k != kProfAttn + 1) return;
   (void)hipEventRecord(g_prof.ev[kProfEvents * call + k], s);
 }
 
@@ -579,11 +582,12 @@ evisel_status evisel_frame_evidence(const evisel_mask* m,
   return EVISEL_OK;
 }
 
-evisel_status evisel_profile_begin(int32_t capacity) {
+evisel_status evisel_profile_begin(int32_t capacity, int32_t all_kernels) {
   if (capacity < 1) return fail(EVISEL_ERR_INVALID_ARG, "capacity < 1");
   if (g_prof.open)
     return fail(EVISEL_ERR_INVALID_ARG, "a profiling session is open");
   g_prof = Profile();
+  g_prof.all = all_kernels != 0;
   try {
     g_prof.ev.resize((size_t)capacity * kProfEvents);
   } catch (const std::bad_alloc&) {
@@ -609,8 +613,10 @@ evisel_status evisel_profile_end(double* ms, int64_t* n_calls) {
   hipError_t err = hipSuccess;
   for (size_t c = 0; c < g_prof.used && err == hipSuccess; ++c) {
     const hipEvent_t* ev = &g_prof.ev[kProfEvents * c];
-    err = hipEventSynchronize(ev[kSpans]);
-    for (int k = 0; k < kSpans && err == hipSuccess; ++k) {
+    const int k0 = g_prof.all ? 0 : kProfAttn;
+    const int k1 = g_prof.all ? kSpans : kProfAttn + 1;
+    err = hipEventSynchronize(ev[k1]);
+    for (int k = k0; k < k1 && err == hipSuccess; ++k) {
       float t = 0.f;
       err = hipEventElapsedTime(&t, ev[k], ev[k + 1]);
       acc[k] += t;
