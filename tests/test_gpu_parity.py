@@ -210,6 +210,26 @@ def test_deterministic_bitwise():
     assert np.array_equal(a.text_mass, b.text_mass)
 
 
+def test_profile_sessions():
+    """Kernel timing: with all_kernels the five spans are recorded; without,
+    only the attention kernel's, and the others read 0."""
+    w = wl.get(2)
+    say("case profile sessions")
+    for all_kernels in (False, True):
+        pytest.ev.profile_begin(4, all_kernels=all_kernels)
+        try:
+            run_gpu(pytest.ev, w, [0, 0], keep_o=False)   # two calls
+        finally:
+            prof = pytest.ev.profile_end()
+        assert prof["calls"] == 2 and prof["attention_ms"] > 0
+        others = [prof[k] for k in ("combine_ms", "evidence_ms")]
+        if all_kernels:
+            assert all(x > 0 for x in others)
+        else:
+            assert others == [0.0, 0.0] and prof["select_ms"] == 0.0
+            assert prof["cues_ms"] == 0.0
+
+
 def test_onehot_values_reproduce_evidence():
     """V = one-hot(frame) on visual keys, 0 elsewhere: the query rows'
     outputs summed over rows equal the separately reduced evidence."""
