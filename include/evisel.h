@@ -103,6 +103,7 @@ typedef struct {
   float tau_p;             /* the rule's tau_p                            */
   int64_t n_frame_pairs;   /* (frame, earlier frame) pairs the pattern can
                               connect: entries of the cross-frame cue      */
+  int64_t n_paired_tiles;  /* key tiles of paired work items (below)      */
 } evisel_mask_stats;
 
 /* Builds the block partition, the compact list of active block pairs (CSR,
@@ -143,11 +144,28 @@ evisel_status evisel_mask_export(const evisel_mask* mask, int32_t* blk_start,
  * query block (-1 for padding), first query head, number of query heads
  * (consecutive, sharing one kv head), first and one-past-last CSR position
  * of its key blocks, and the first head's split slot (-1 unless the item is
- * part of a split query-token row). Any pointer may be NULL. */
+ * part of a split query-token row). Any pointer may be NULL.
+ * With the static rule and an odd number of query heads per kv head, the
+ * odd head of a kv group is covered by paired items: one head over two
+ * query blocks of the same video and region (qblock and qblock2 >= 0; for
+ * split query-token rows, the same chunk of two consecutive query-token
+ * blocks, with slots slot and slot2). A paired item's [kb_begin, kb_end)
+ * indexes the paired-tile list of evisel_mask_export_paired instead of the
+ * CSR. qblock2 and slot2 are -1 for every other item. */
 evisel_status evisel_mask_export_work(const evisel_mask* mask, int32_t* qblock,
                                       int32_t* head, int32_t* nheads,
                                       int32_t* kb_begin, int32_t* kb_end,
-                                      int32_t* slot);
+                                      int32_t* slot, int32_t* qblock2,
+                                      int32_t* slot2);
+
+/* Copies the paired-tile list (n_paired_tiles entries): the key block and
+ * its CSR position in the row of the paired item's first and second query
+ * block (-1 where the key block is not active for that query block). The
+ * tiles of one item are in increasing key-block order and are the union of
+ * the two blocks' CSR runs. Any pointer may be NULL. */
+evisel_status evisel_mask_export_paired(const evisel_mask* mask,
+                                        int32_t* block, int32_t* pos_a,
+                                        int32_t* pos_b);
 
 /* Bytes of device workspace evisel_sparse_prefill (and, for a top-p mask,
  * evisel_select_blocks) needs for head dim d. */

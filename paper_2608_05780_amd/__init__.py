@@ -10,7 +10,8 @@ Entry points (same names as the C ABI):
     select_blocks          top-p masks: per-row retained history blocks
     sparse_prefill         one layer: attention output, LSE, evidence slice
     frame_evidence         head/layer aggregation and per-video top-k frames
-    sparse_prefill_workspace, mask_info, mask_export, mask_export_work
+    sparse_prefill_workspace, mask_info, mask_export, mask_export_work,
+    mask_export_paired     plan inspection (host tables)
 """
 from __future__ import annotations
 
@@ -22,7 +23,8 @@ __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "sparse_prefill_workspace", "sparse_prefill", "frame_evidence",
            "select_blocks", "unpack_row_bits", "mask_export_pairs",
            "coarse_evidence",
-           "mask_info", "mask_export", "mask_export_work", "profile_begin",
+           "mask_info", "mask_export", "mask_export_work",
+           "mask_export_paired", "profile_begin",
            "profile_end", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)),
@@ -51,7 +53,8 @@ class _Stats(ctypes.Structure):
         "n_active_pairs", "n_work_items", "n_text_tiles", "n_chunk_slots")] + \
         [(n, ctypes.c_int32) for n in ("hq", "hkv", "block",
                                        "tokens_per_frame", "hist_words")] + \
-        [("tau_p", ctypes.c_float), ("n_frame_pairs", ctypes.c_int64)]
+        [("tau_p", ctypes.c_float), ("n_frame_pairs", ctypes.c_int64),
+         ("n_paired_tiles", ctypes.c_int64)]
 
 
 _lib = None
@@ -69,7 +72,8 @@ _SIGS = {
     "evisel_mask_info": (ctypes.c_int, [ctypes.c_void_p,
                                         ctypes.POINTER(_Stats)]),
     "evisel_mask_export": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 6),
-    "evisel_mask_export_work": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 6),
+    "evisel_mask_export_work": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 8),
+    "evisel_mask_export_paired": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 3),
     "evisel_sparse_prefill_workspace": (ctypes.c_size_t, [ctypes.c_void_p,
                                                           ctypes.c_int32]),
     "evisel_sparse_prefill": (ctypes.c_int, [
@@ -221,12 +225,25 @@ def mask_export(mask: Mask) -> dict:
 def mask_export_work(mask: Mask) -> dict:
     import numpy as np
     n = mask.stats["n_work_items"]
-    out = {k: np.zeros(max(n, 1), np.int32) for k in (
-        "qblock", "head", "nheads", "kb_begin", "kb_end", "slot")}
+    keys = ("qblock", "head", "nheads", "kb_begin", "kb_end", "slot",
+            "qblock2", "slot2")
+    out = {k: np.zeros(max(n, 1), np.int32) for k in keys}
     p = lambda a: a.ctypes.data_as(_i32p)
-    _check(load().evisel_mask_export_work(
-        mask.handle, p(out["qblock"]), p(out["head"]), p(out["nheads"]),
-        p(out["kb_begin"]), p(out["kb_end"]), p(out["slot"])))
+    _check(load().evisel_mask_export_work(mask.handle,
+                                          *[p(out[k]) for k in keys]))
+    return {k: v[:n] for k, v in out.items()}
+
+
+def mask_export_paired(mask: Mask) -> dict:
+    """Key tiles of paired work items: key block and its CSR position in
+    the first / second query block's row (-1: not active there)."""
+    import numpy as np
+    n = mask.stats["n_paired_tiles"]
+    keys = ("block", "pos_a", "pos_b")
+    out = {k: np.zeros(max(n, 1), np.int32) for k in keys}
+    p = lambda a: a.ctypes.data_as(_i32p)
+    _check(load().evisel_mask_export_paired(mask.handle,
+                                            *[p(out[k]) for k in keys]))
     return {k: v[:n] for k, v in out.items()}
 
 

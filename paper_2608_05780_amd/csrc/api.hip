@@ -94,8 +94,9 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   const evisel::Plan& P = m->plan;
   std::vector<char> buf;
   const size_t o_blk = put(buf, P.blocks), o_col = put(buf, P.col),
-               o_cd = put(buf, P.col_desc),
-               o_it = put(buf, P.items), o_seq = put(buf, P.seqs),
+               o_cd = put(buf, P.col_desc), o_pt = put(buf, P.ptile),
+               o_pd = put(buf, P.ptile_desc), o_it = put(buf, P.items),
+               o_seq = put(buf, P.seqs),
                o_tt = put(buf, P.tiles), o_fs = put(buf, P.frame_seq),
                o_bl = put(buf, P.blk_local), o_fp = put(buf, P.pairs),
                o_fop = put(buf, P.ff_out_ptr), o_foi = put(buf, P.ff_out_idx),
@@ -116,6 +117,8 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
   dp.blocks = (const evisel::BlockDesc*)(d + o_blk);
   dp.col = (const int32_t*)(d + o_col);
   dp.col_desc = (const evisel::BlockDesc*)(d + o_cd);
+  dp.ptile = (const evisel::PairedTile*)(d + o_pt);
+  dp.ptile_desc = (const evisel::BlockDesc*)(d + o_pd);
   dp.items = (const evisel::WorkItem*)(d + o_it);
   dp.seqs = (const evisel::SeqDesc*)(d + o_seq);
   dp.tiles = (const evisel::TextTile*)(d + o_tt);
@@ -337,6 +340,7 @@ evisel_status evisel_mask_info(const evisel_mask* m, evisel_mask_stats* out) {
   out->hist_words = P.hist_words;
   out->tau_p = P.rule.tau;
   out->n_frame_pairs = (int64_t)P.pairs.size();
+  out->n_paired_tiles = (int64_t)P.ptile.size();
   return EVISEL_OK;
 }
 
@@ -366,7 +370,8 @@ evisel_status evisel_mask_export(const evisel_mask* m, int32_t* blk_start,
 evisel_status evisel_mask_export_work(const evisel_mask* m, int32_t* qblock,
                                       int32_t* head, int32_t* nheads,
                                       int32_t* kb_begin, int32_t* kb_end,
-                                      int32_t* slot) {
+                                      int32_t* slot, int32_t* qblock2,
+                                      int32_t* slot2) {
   if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
   const auto& it = m->plan.items;
   for (size_t i = 0; i < it.size(); ++i) {
@@ -376,6 +381,20 @@ evisel_status evisel_mask_export_work(const evisel_mask* m, int32_t* qblock,
     if (kb_begin) kb_begin[i] = it[i].kb_begin;
     if (kb_end) kb_end[i] = it[i].kb_end;
     if (slot) slot[i] = it[i].slot;
+    if (qblock2) qblock2[i] = it[i].qblock2;
+    if (slot2) slot2[i] = it[i].slot2;
+  }
+  return EVISEL_OK;
+}
+
+evisel_status evisel_mask_export_paired(const evisel_mask* m, int32_t* block,
+                                        int32_t* pos_a, int32_t* pos_b) {
+  if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
+  const auto& pt = m->plan.ptile;
+  for (size_t i = 0; i < pt.size(); ++i) {
+    if (block) block[i] = pt[i].block;
+    if (pos_a) pos_a[i] = pt[i].pos[0];
+    if (pos_b) pos_b[i] = pt[i].pos[1];
   }
   return EVISEL_OK;
 }

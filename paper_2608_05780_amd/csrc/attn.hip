@@ -8,6 +8,11 @@
 // is staged once in LDS for both heads. Two work-groups fit a CU, so every
 // SIMD interleaves two wavefronts and part of one's softmax VALU work hides
 // under the other's MFMAs.
+// A kv group with an odd number of query heads (7 for 28/4) leaves one head
+// over; it runs as paired items, in which waves 2-3 take a second query
+// block for the same head (the region's next block, or the same chunk of the
+// video's next query-token block). The item's key tiles are the two blocks'
+// lists merged, and each half computes only the tiles active for its rows.
 //
 // Key/value tiles go straight from global memory to LDS (16-byte
 // global_load_lds per lane, no staging registers), double-buffered: tile j+1
@@ -288,15 +293,17 @@ struct Bf16Path {
   static constexpr int kPer = kTile * RC / kThreads;   // chunks per thread
 
   // Staged Q in two halves, so that its global loads share a round trip
-  // with the first tile's: stage_q_load reads rows [start, start+len) of
-  // heads h0 and, when nh is 2, h0+1 into registers (rows past len repeat
-  // the last row), stage_q_store writes them to d0 / d1 (rows past len as
-  // zeros).
+  // with the first tile's: stage_q_load reads, for half hh < nh, rows
+  // [start[hh], start[hh]+len[hh]) of head hd[hh] into registers (rows past
+  // len repeat the last row), stage_q_store writes them to d0 / d1 (rows
+  // past len as zeros).
   struct QStage {
     bf16x8 v[2][kPer];
   };
-  __device__ static void stage_q_load(QStage& st, const void* q, int start,
-                                      int len, int h0, int nh, int hq,
+  __device__ static void stage_q_load(QStage& st, const void* q,
+                                      const int (&start)[2],
+                                      const int (&len)[2],
+                                      const int (&hd)[2], int nh, int hq,
                                       int tid) {
     const __bf16* src = (const __bf16*)q;
 #pragma unroll
@@ -305,16 +312,16 @@ struct Bf16Path {
 #pragma unroll
         for (int i = 0; i < kPer; ++i) {
           const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
-          const int r = min(row, len - 1);
-          st.v[hh][i] = *(const bf16x8*)(src + ((size_t)(start + r) * hq +
-                                                h0 + hh) * D + ch * 8);
+          const int r = min(row, len[hh] - 1);
+          st.v[hh][i] = *(const bf16x8*)(src + ((size_t)(start[hh] + r) * hq +
+                                                hd[hh]) * D + ch * 8);
         }
       }
     }
   }
   __device__ static void stage_q_store(const QStage& st, EV_LDS char* d0,
-                                       EV_LDS char* d1, int len, int nh,
-                                       int tid) {
+                                       EV_LDS char* d1, const int (&len)[2],
+                                       int nh, int tid) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       if (hh < nh) {
@@ -324,7 +331,7 @@ struct Bf16Path {
           const bf16x8 z = {};
           *(EV_LDS bf16x8*)((hh ? d1 : d0) +
                             (row * RC + (ch ^ swz<kSwzK, RC>(row))) * 16) =
-              row < len ? st.v[hh][i] : z;
+              row < len[hh] ? st.v[hh][i] : z;
         }
       }
     }
@@ -433,10 +440,12 @@ struct F32Path {
   }
   static constexpr bool kStaged = false;
   struct QStage {};
-  __device__ static void stage_q_load(QStage&, const void*, int, int, int,
-                                      int, int, int) {}
+  __device__ static void stage_q_load(QStage&, const void*, const int (&)[2],
+                                      const int (&)[2], const int (&)[2], int,
+                                      int, int) {}
   __device__ static void stage_q_store(const QStage&, EV_LDS char*,
-                                       EV_LDS char*, int, int, int) {}
+                                       EV_LDS char*, const int (&)[2], int,
+                                       int) {}
   __device__ static void load_q_lds(QFrag&, const EV_LDS char*, int, int) {}
   __device__ static void o_to_lds(EV_LDS char*, const f32x16 (&)[D / 32],
                                   float, int, int) {}
@@ -464,10 +473,17 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform
   const int l32 = lane & 31, g = lane >> 5;
   const int hsub = wave >> 1;
-  const bool active = hsub < it.nheads;
-  const int h = it.head + (active ? hsub : 0);
+  // A paired item gives the second half of the work-group its own query
+  // block (same head); otherwise the halves take heads head, head + 1.
+  const bool uni = !TOPP && it.qblock2 >= 0;
+  const int nhalf = uni ? 2 : it.nheads;   // halves with rows
+  const bool active = hsub < nhalf;
+  const int hd1 = uni ? it.head : it.head + 1;   // the second half's head
+  const int h = active && hsub ? hd1 : it.head;
   const int kvh = it.head / (pl.hq / pl.hkv);
-  const BlockDesc qb = pl.blocks[it.qblock];
+  const BlockDesc qb0 = pl.blocks[it.qblock];
+  const BlockDesc qb1 = uni ? pl.blocks[it.qblock2] : qb0;
+  const BlockDesc qb = hsub ? qb1 : qb0;
   const bool is_text = it.slot >= 0;
   const int qrow = 32 * (wave & 1) + l32;
   const bool qvalid = active && qrow < qb.len;
@@ -500,7 +516,9 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   // Descriptors of this item's key tiles, 64 at a time: lane t holds the
   // BlockDesc of tile 64*batch + t, and the loop reads tile j's with
   // v_readlane. (Loading them per tile would put two dependent global round
-  // trips in front of every tile's K/V loads.)
+  // trips in front of every tile's K/V loads.) dsc_pos is the tile's CSR
+  // position in the row of the wave's query block (paired items: -1 when
+  // the key block is not active for it).
   // Top-p: dsc_loc is the tile's local history index, or -1 when the tile
   // is always visible.
   int dsc_start = 0, dsc_len = 1, dsc_region = 0, dsc_aux = 0, dsc_loc = -1,
@@ -509,8 +527,9 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     const int t = batch * 64 + lane;
     if (t < n) {
       const int pos = TOPP ? (int)clist[t] : t;
-      const BlockDesc bd = pl.col_desc[b0 + pos];
-      dsc_pos = pos;
+      const BlockDesc bd =
+          uni ? pl.ptile_desc[b0 + t] : pl.col_desc[b0 + pos];
+      dsc_pos = uni ? pl.ptile[b0 + t].pos[hsub] : b0 + pos;
       dsc_start = bd.start;
       dsc_len = bd.len;
       dsc_region = bd.region;
@@ -539,8 +558,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   if constexpr (!TOPP) load_batch(0);
   typename P::QStage qst;
   if constexpr (P::kStaged)
-    P::stage_q_load(qst, ac.q, qb.start, qb.len, it.head, it.nheads, pl.hq,
-                    tid);
+    P::stage_q_load(qst, ac.q, {qb0.start, qb1.start}, {qb0.len, qb1.len},
+                    {it.head, hd1}, nhalf, pl.hq, tid);
 
   // Top-p: a candidate tile is kept when it is always visible (system
   // prefix, the query block itself) or some row of the item's heads
@@ -654,7 +673,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       if (cur.region == kVis && pl.Nv == kTile) {
         // one frame per key tile: its partial is the row's tile sum
         float* dst = is_text ? seg_row + cur.aux
-                             : segv_row + (size_t)(b0 + cpos) * kTile;
+                             : segv_row + (size_t)cpos * kTile;
         const float t = pair_sum(ts);
         if (g == 0 && qvalid) *dst = mu + log2_(t);
       } else if (cur.region == kVis) {
@@ -671,7 +690,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         const int lg = __builtin_ctz((unsigned)pl.Nv) - 3;  // log2(N_v / 8)
         const int nseg = kTile / pl.Nv;
         float* dst = is_text ? seg_row + cur.aux
-                             : segv_row + (size_t)(b0 + cpos) * fpt * kTile;
+                             : segv_row + (size_t)cpos * fpt * kTile;
         const int dstride = is_text ? 1 : kTile;
         for (int si = 0; si < nseg; ++si) {
           float t = 0.f;
@@ -698,8 +717,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   auto loc_of = [&](int t) {
     return TOPP ? __builtin_amdgcn_readlane(dsc_loc, t & 63) : -1;
   };
-  auto pos_of = [&](int t) {   // CSR offset of compacted tile t
-    return TOPP ? __builtin_amdgcn_readlane(dsc_pos, t & 63) : t;
+  auto pos_of = [&](int t) {   // CSR position of tile t for the wave's rows
+    return TOPP || uni ? __builtin_amdgcn_readlane(dsc_pos, t & 63) : b0 + t;
   };
 
   // Tile j+1 streams into the other buffer pair while tile j is computed.
@@ -713,7 +732,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     if (TOPP) wnext = row_bits(lnext);
   }
   if constexpr (P::kStaged) {
-    P::stage_q_store(qst, kbuf(1), vbuf(1), qb.len, it.nheads, tid);
+    P::stage_q_store(qst, kbuf(1), vbuf(1), {qb0.len, qb1.len}, nhalf, tid);
     __syncthreads();   // staged Q visible to every wave
     P::load_q_lds(qf, hsub ? vbuf(1) : kbuf(1), qrow, g);
   }
@@ -734,7 +753,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       }
       pnext = pos_of(j + 1);
     }
-    if (active) {
+    if (active && pcur >= 0) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
       P::qk(s, kbuf(j), qf, l32, g);
       tile_pre(s, cur, wcur, lcur);
@@ -749,8 +768,9 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     __syncthreads();   // every wave is done with the last tile
     if (active) P::o_to_lds(kbuf(hsub), o, qvalid ? 1.f / l_tot : 0.f, qrow, g);
     __syncthreads();
-    for (int hh = 0; hh < it.nheads; ++hh)
-      P::o_from_lds(ac.o, kbuf(hh), qb.start, qb.len, it.head + hh, pl.hq, tid);
+    for (int hh = 0; hh < nhalf; ++hh)
+      P::o_from_lds(ac.o, kbuf(hh), hh ? qb1.start : qb0.start,
+                    hh ? qb1.len : qb0.len, hh ? hd1 : it.head, pl.hq, tid);
   }
   if (!active) return;
 
@@ -774,7 +794,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     }
   } else {
     const float nv_tot = pair_sum(nv_part);
-    const int slot = it.slot + hsub * it.nch;
+    const int slot =
+        uni ? (hsub ? it.slot2 : it.slot) : it.slot + hsub * it.nch;
     if (qvalid) {
       float* po = ws.pO + ((size_t)slot * kTile + qrow) * D;
 #pragma unroll

@@ -12,6 +12,8 @@ struct DevPlan {
   const int32_t* col;
   const BlockDesc* col_desc;  // [nnz] descriptor of each CSR entry's block
   const WorkItem* items;
+  const PairedTile* ptile;       // key tiles of paired items
+  const BlockDesc* ptile_desc;   // descriptor of each paired tile's block
   const SeqDesc* seqs;
   const TextTile* tiles;
   const int32_t* frame_seq;

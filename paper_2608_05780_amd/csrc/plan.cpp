@@ -11,6 +11,7 @@
 #include "plan.h"
 
 #include <algorithm>
+#include <limits>
 #include <map>
 #include <numeric>
 
@@ -199,50 +200,116 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   const int64_t avg = (total + kTargetSlots - 1) / kTargetSlots;
   P.chunk_blocks = (int32_t)std::max<int64_t>(16, avg);
 
+  // Paired items (static rule only: top-p items select per row against
+  // their own block's history): the kv group's odd head takes two query
+  // blocks in one item. Both CSR rows are in ascending key-block order, so
+  // their runs merge by key block.
+  const bool pair_rows = !topp;
+  auto paired = [&](int32_t qa, int32_t a0, int32_t a1, int32_t qb2,
+                    int32_t c0, int32_t c1, int32_t h, int32_t slot_a,
+                    int32_t slot_b, int32_t n, int32_t nch) {
+    const int32_t begin = (int32_t)P.ptile.size();
+    const int32_t none = std::numeric_limits<int32_t>::max();
+    int32_t i = a0, j = c0;
+    while (i < a1 || j < c1) {
+      const int32_t ka = i < a1 ? P.col[i] : none;
+      const int32_t kb = j < c1 ? P.col[j] : none;
+      PairedTile t;
+      t.block = std::min(ka, kb);
+      t.pos[0] = ka == t.block ? i++ : -1;
+      t.pos[1] = kb == t.block ? j++ : -1;
+      P.ptile.push_back(t);
+    }
+    return WorkItem{qa, h,     1,  begin, (int32_t)P.ptile.size(),
+                    slot_a, n, nch, qb2,  slot_b};
+  };
+
   std::vector<Item> txt_items, other_items;
   for (size_t n = 0; n < nseq; ++n) {
+    // query-token tiles of this video and their chunk slots
+    struct Tile {
+      int32_t b, rb, len, nch, slot0;
+    };
+    std::vector<Tile> vt;
     for (int32_t b : txtb[n]) {
-      const int32_t rb = P.row_ptr[b], re = P.row_ptr[b + 1];
-      const int32_t len = re - rb;
+      const int32_t rb = P.row_ptr[b], len = P.row_ptr[b + 1] - rb;
       const int32_t nch = (len + P.chunk_blocks - 1) / P.chunk_blocks;
       TextTile tt{b, (int32_t)n, nch, (int32_t)P.n_slots};
       if (P.seqs[n].n_tiles == 0) P.seqs[n].tile0 = (int32_t)P.tiles.size();
       P.seqs[n].n_tiles++;
       P.tiles.push_back(tt);
+      vt.push_back({b, rb, len, nch, tt.slot0});
+      P.n_slots += (int64_t)hq * nch;
+    }
+    // equal-size chunks: chunk c of a tile covers [rb + c*len/nch, ...)
+    auto lo = [](const Tile& t, int32_t c) {
+      return t.rb + (int32_t)((int64_t)c * t.len / t.nch);
+    };
+    for (size_t ti = 0; ti < vt.size(); ++ti) {
+      const Tile& t = vt[ti];
       for (int32_t g = 0; g < hkv; ++g)
         for (int32_t pp = 0; pp < pairs; ++pp) {
           const int32_t h0 = g * group + pp * kHeadsPerItem;
           const int32_t nh = std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
-          for (int32_t c = 0; c < nch; ++c) {
-            // equal-size chunks: chunk c covers [rb + c*len/nch, ...)
-            const int32_t a = rb + (int32_t)((int64_t)c * len / nch);
-            const int32_t e = rb + (int32_t)((int64_t)(c + 1) * len / nch);
-            WorkItem w{b, h0, nh, a, e, tt.slot0 + h0 * nch + c, (int32_t)n,
-                       nch};
-            txt_items.push_back(
-                {w, e - a + 1, ((int64_t)n * hkv + g) * 65536 + c});
+          const bool pr = nh == 1 && pair_rows;
+          // odd head: chunk c of tiles 2i and 2i+1 share one item
+          const int32_t c_first =
+              pr && ti % 2 == 1 ? std::min(vt[ti - 1].nch, t.nch) : 0;
+          for (int32_t c = c_first; c < t.nch; ++c) {
+            const int64_t key = ((int64_t)n * hkv + g) * 65536 + c;
+            if (pr && ti % 2 == 0 && ti + 1 < vt.size() &&
+                c < vt[ti + 1].nch) {
+              const Tile& u = vt[ti + 1];
+              const WorkItem w = paired(
+                  t.b, lo(t, c), lo(t, c + 1), u.b, lo(u, c), lo(u, c + 1),
+                  h0, t.slot0 + h0 * t.nch + c, u.slot0 + h0 * u.nch + c,
+                  (int32_t)n, t.nch);
+              txt_items.push_back({w, w.kb_end - w.kb_begin + 1, key});
+              continue;
+            }
+            const WorkItem w{t.b, h0, nh, lo(t, c), lo(t, c + 1),
+                             t.slot0 + h0 * t.nch + c, (int32_t)n, t.nch,
+                             -1, -1};
+            txt_items.push_back({w, w.kb_end - w.kb_begin + 1, key});
           }
         }
-      P.n_slots += (int64_t)hq * nch;
     }
     // visual and system rows, ordered by (kv head, block, head pair) so that
     // neighbouring launches share key/value tiles
     for (int32_t g = 0; g < hkv; ++g) {
       auto add = [&](const std::vector<int32_t>& ids) {
-        for (int32_t b : ids)
+        for (size_t i = 0; i < ids.size(); ++i) {
+          const int32_t b = ids[i];
           for (int32_t pp = 0; pp < pairs; ++pp) {
             const int32_t h0 = g * group + pp * kHeadsPerItem;
             const int32_t nh =
                 std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
-            WorkItem w{b, h0, nh, P.row_ptr[b], P.row_ptr[b + 1], -1,
-                       (int32_t)n, 0};
+            if (nh == 1 && pair_rows) {
+              // odd head: blocks 2i and 2i+1 of the region share one item
+              if (i % 2 == 1) continue;
+              if (i + 1 < ids.size()) {
+                const int32_t b2 = ids[i + 1];
+                const WorkItem w =
+                    paired(b, P.row_ptr[b], P.row_ptr[b + 1], b2,
+                           P.row_ptr[b2], P.row_ptr[b2 + 1], h0, -1, -1,
+                           (int32_t)n, 0);
+                other_items.push_back({w, w.kb_end - w.kb_begin + 1});
+                continue;
+              }
+            }
+            const WorkItem w{b, h0, nh, P.row_ptr[b], P.row_ptr[b + 1], -1,
+                             (int32_t)n, 0, -1, -1};
             other_items.push_back({w, P.row_ptr[b + 1] - P.row_ptr[b] + 1});
           }
+        }
       };
       add(sysb[n]);
       add(visb[n]);
     }
   }
+  P.ptile_desc.resize(P.ptile.size());
+  for (size_t i = 0; i < P.ptile.size(); ++i)
+    P.ptile_desc[i] = P.blocks[P.ptile[i].block];
 
   // Longest-first over the XCD queues: split query-token items go first, by
   // LPT; the remaining items keep their locality order and are cut into
@@ -300,7 +367,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
       if (r < q[x].size()) {
         P.items.push_back(q[x][r]);
       } else {
-        WorkItem pad{-1, 0, 0, 0, 0, -1, 0, 0};
+        WorkItem pad{-1, 0, 0, 0, 0, -1, 0, 0, -1, -1};
         P.items.push_back(pad);
       }
     }

@@ -41,15 +41,29 @@ constexpr int kHeadsPerItem = 2;
 // query heads of one kv head, and a contiguous run of the block's CSR row.
 // Items of split query-token rows carry the first head's partial slot; head
 // head+i uses slot + i*nch.
+// A paired item (qblock2 >= 0) holds a single head for two query blocks of
+// one video and region, qblock for the first half of the work-group and
+// qblock2 for the second, so that the odd head of a kv group does not leave
+// half a work-group idle. Its key tiles are the two blocks' CSR runs merged
+// by key block: entries [kb_begin, kb_end) of the paired-tile list.
 struct WorkItem {
   int32_t qblock;    // -1: padding, exits immediately
   int32_t head;      // first query head
-  int32_t nheads;    // 1..kHeadsPerItem
-  int32_t kb_begin;  // CSR positions [kb_begin, kb_end)
+  int32_t nheads;    // 1..kHeadsPerItem (1 for a paired item)
+  int32_t kb_begin;  // CSR positions [kb_begin, kb_end) (paired: tiles)
   int32_t kb_end;
   int32_t slot;      // -1 for visual/system rows; else first head's slot
   int32_t seq;       // video of the query block
   int32_t nch;       // chunks of this query-token row (0 for other rows)
+  int32_t qblock2;   // -1, or the second query block of a paired item
+  int32_t slot2;     // paired query-token item: qblock2's slot, else -1
+};
+
+// Key tile of a paired item: the key block and its CSR position in the row
+// of each of the two query blocks (-1: not active for that query block).
+struct PairedTile {
+  int32_t block;
+  int32_t pos[2];
 };
 
 // A query-token block and its chunk slots: slot(h, c) = slot0 + h*n_chunks + c.
@@ -102,6 +116,8 @@ struct Plan {
   std::vector<int32_t> row_ptr, col;
   std::vector<BlockDesc> col_desc;  // [nnz] descriptor of col[p]'s block
   std::vector<WorkItem> items;      // launch order
+  std::vector<PairedTile> ptile;    // key tiles of paired items
+  std::vector<BlockDesc> ptile_desc;  // descriptor of ptile[i].block
   std::vector<SeqDesc> seqs;
   std::vector<TextTile> tiles;
   std::vector<int32_t> frame_seq;   // [T] video of each global frame

@@ -84,30 +84,105 @@ def test_workload_plans(lib, cid):
     _check_work(m, got, w.hq)
 
 
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (6, 2), (2, 2), (8, 2)])
+def test_odd_heads_are_paired(lib, hq, hkv):
+    """With an odd number of query heads per kv head, the odd head of each
+    group runs as paired items (two query blocks per work-group): every
+    region with two or more blocks pairs them, query-token tiles pair chunk
+    by chunk, and only a region's last odd block stays alone. Even groups
+    and top-p masks have no paired items."""
+    ns, nf, nt, Nv, rule = CASES[2]
+    m = _plan(nf, nt, Nv, rule, hq=hq, hkv=hkv, n_sys=ns)
+    got = ev.mask_export(m)
+    _check_work(m, got, hq)
+    wk = ev.mask_export_work(m)
+    group = hq // hkv
+    n_paired = int((wk["qblock2"] >= 0).sum())
+    if group % 2 == 0:
+        assert n_paired == 0 and m.stats["n_paired_tiles"] == 0
+    else:
+        region, video = got["region"], got["video"]
+        odd = {}
+        for idx, qb, h0, nh, run, s in _work_units(m, got, hq):
+            if h0 % group == group - 1:
+                odd.setdefault((qb, h0), []).append(idx)
+        paired_blocks = {}
+        for qb, q2, h0 in zip(wk["qblock"], wk["qblock2"], wk["head"]):
+            if q2 >= 0:
+                paired_blocks.setdefault(int(h0), set()).update(
+                    (int(qb), int(q2)))
+        for g in range(hkv):
+            h = g * group + group - 1
+            for n in range(len(nf)):
+                for r in (0, 1, 2):
+                    ids = np.nonzero((video == n) & (region == r))[0]
+                    lone = set(ids.tolist()) - paired_blocks.get(h, set())
+                    assert len(lone) == len(ids) % 2, (h, n, r, lone)
+                    if lone:
+                        assert lone == {int(ids[-1])}
+        assert n_paired > 0
+    mt = _plan(nf, nt, Nv, rule, hq=hq, hkv=hkv, n_sys=ns, tau_p=0.97)
+    assert (ev.mask_export_work(mt)["qblock2"] < 0).all()
+    assert mt.stats["n_paired_tiles"] == 0
+
+
+def _work_units(m, csr, hq):
+    """The work list as (launch index, query block, first head, heads, CSR
+    run, slot) units: an ordinary item is one unit; a paired item (the odd
+    head of a kv group over two query blocks of one video and region) is
+    one unit per query block, whose CSR run is read back from its tiles.
+    Checks that a paired item's tiles are the two runs merged by key block."""
+    wk = ev.mask_export_work(m)
+    pt = ev.mask_export_paired(m)
+    region, col = csr["region"], csr["col"]
+    group = hq // m.stats["hkv"]
+    units = []
+    for idx, (qb, h0, nh, a, e, s, q2, s2) in enumerate(zip(
+            wk["qblock"], wk["head"], wk["nheads"], wk["kb_begin"],
+            wk["kb_end"], wk["slot"], wk["qblock2"], wk["slot2"])):
+        if qb < 0:
+            continue
+        if q2 < 0:
+            assert s2 == -1
+            units.append((idx, int(qb), int(h0), int(nh), (int(a), int(e)),
+                          int(s)))
+            continue
+        assert nh == 1 and group % 2 == 1 and h0 % group == group - 1
+        assert csr["video"][qb] == csr["video"][q2]
+        assert region[qb] == region[q2] and qb != q2
+        assert (s2 >= 0) == (s >= 0) == (region[qb] == 2)
+        blocks = pt["block"][a:e]
+        assert len(blocks) > 0 and np.all(np.diff(blocks) > 0)
+        pa, pb = pt["pos_a"][a:e], pt["pos_b"][a:e]
+        assert np.all((pa >= 0) | (pb >= 0))
+        for q, pos, sl in ((qb, pa, s), (q2, pb, s2)):
+            p = pos[pos >= 0]
+            assert len(p) > 0 and np.all(np.diff(p) == 1)   # one run
+            np.testing.assert_array_equal(col[p], blocks[pos >= 0])
+            units.append((idx, int(q), int(h0), 1, (int(p[0]), int(p[-1]) + 1),
+                          int(sl)))
+    return units
+
+
 def _check_work(m, csr, hq):
     """Every (query block, head) is covered exactly once by contiguous runs of
     its CSR row; heads of an item share a kv head; query-token items use
     distinct slots that exactly fill [0, n_chunk_slots); the query-token
     chunks that read the same key range (same video, kv head and chunk
     index) are launched on one XCD (work-group i runs on XCD i mod 8)."""
-    wk = ev.mask_export_work(m)
     region, rp = csr["region"], csr["row_ptr"]
     group = hq // m.stats["hkv"]
     seen, text_items = {}, []
     xcd_of = {}
-    for idx, (qb, h0, nh, a, e, s) in enumerate(zip(
-            wk["qblock"], wk["head"], wk["nheads"], wk["kb_begin"],
-            wk["kb_end"], wk["slot"])):
-        if qb < 0:
-            continue
+    for idx, qb, h0, nh, (a, e), s in _work_units(m, csr, hq):
         if region[qb] == 2:
-            xcd_of[(int(qb), int(h0), int(a))] = idx % 8
+            xcd_of[(qb, h0, a)] = idx % 8
         assert rp[qb] <= a < e <= rp[qb + 1]
         assert 1 <= nh <= 4 and h0 // group == (h0 + nh - 1) // group
         for i in range(nh):
-            seen.setdefault((int(qb), int(h0 + i)), []).append((int(a), int(e)))
+            seen.setdefault((qb, h0 + i), []).append((a, e))
         if region[qb] == 2:
-            text_items.append((int(qb), int(h0), int(nh), int(s)))
+            text_items.append((qb, h0, nh, s))
         else:
             assert s == -1 and (a, e) == (rp[qb], rp[qb + 1])
     assert len(seen) == len(region) * hq
