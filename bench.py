@@ -39,18 +39,32 @@ PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 2.4 GHz x 4096 flop/clk (dense)
 PEAK_HBM_GBS = 8000.0
 
 
+# Sources whose change invalidates the committed counter figures: the
+# attention kernel and the plan that orders its work (launch order decides
+# how much of the key/value traffic each XCD's L2 absorbs).
+TRAFFIC_SOURCES = ("attn.hip", "plan.cpp", "plan.h")
+
+
+def traffic_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2608_05780_amd", "csrc", f),
+                      "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per attention launch from the committed counter summary,
-    or None when the attention source changed since it was measured."""
-    import hashlib
-    src = os.path.join(ROOT, "paper_2608_05780_amd", "csrc", "attn.hip")
+    or None when the attention kernel or the plan changed since it was
+    measured."""
     summ = os.path.join(ROOT, "profiles", "attn_kernel_16k28L_hbm_counters.md")
     try:
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        sha = traffic_source_sha()
         for line in open(summ):
             if line.startswith("traffic_per_launch"):
                 kv = dict(x.split("=") for x in line.split()[1:])
-                if kv["attn_source_sha256"] == sha:
+                if kv["source_sha256"] == sha:
                     return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
     except (OSError, KeyError, ValueError):
         pass

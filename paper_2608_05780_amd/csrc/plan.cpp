@@ -352,11 +352,15 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
       ++pos;
     }
   }
-  // longest first inside each queue (stable: locality order kept per cost)
+  // longest first inside each queue, by length class of 16 key tiles
+  // (stable: items of one class keep their locality order; sorting by the
+  // exact length would move the 11-tile paired visual items away from their
+  // 10-tile neighbours and cost the L2 their shared key/value tiles)
   for (int x = 0; x < kXcds; ++x) {
     std::stable_sort(q[x].begin(), q[x].end(),
                      [](const WorkItem& a, const WorkItem& b) {
-                       return (a.kb_end - a.kb_begin) > (b.kb_end - b.kb_begin);
+                       return (a.kb_end - a.kb_begin + 15) / 16 >
+                              (b.kb_end - b.kb_begin + 15) / 16;
                      });
   }
   size_t rounds = 0;
