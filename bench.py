@@ -15,9 +15,10 @@ aggregation and top-16 frames). Inputs are resident in HBM before timing.
 Prints one JSON line: probe tokens/s (value), ms per step, the attention
 kernel's roofline against the bf16 MFMA peak (active-block FLOPs over the
 kernel's HIP-event time, measured over the timed region, where only that
-kernel is bracketed by events), the other kernels' times from two further
-untimed steps, and the fp64 CPU oracle's throughput on a bounded sample
-(whole layers, at least 10 s) as a baseline.
+kernel is bracketed by events, on every 9th prefill call), the other
+kernels' times from two further untimed steps, and the fp64 CPU oracle's
+throughput on a bounded sample (whole layers, at least 10 s) as a
+baseline.
 
 ``--tau-p P`` runs the same workload under the paper's adaptive top-p
 retention instead of the static rule: every layer first selects each row's
@@ -275,10 +276,14 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # Timed region: HIP events around the attention kernel only (each event
-    # is a dependency packet between kernels, so the others run back to
-    # back); the per-kernel breakdown comes from two further, untimed steps.
-    ev.profile_begin(args.steps * L, all_kernels=False)
+    # Timed region: HIP events around the attention kernel only, and only
+    # on every `stride`-th prefill call: each event is a dependency packet
+    # that idles the GPU for several microseconds, so bracketing every
+    # launch would lengthen the step by about 5 %. The per-kernel breakdown
+    # comes from two further, untimed steps.
+    calls = args.steps * L
+    stride = max(1, min(9, calls // 4))
+    ev.profile_begin(-(-calls // stride), all_kernels=False, stride=stride)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -334,7 +339,8 @@ def main():
                                  w.tau_p == 0 and not args.cues else None),
                      "kernel": "attn_kernel<Bf16Path<128>>",
                      "flop_per_launch": flop_layer,
-                     "avg_launch_ms": attn_ms},
+                     "avg_launch_ms": attn_ms,
+                     "timed_launches": prof_attn["calls"]},
         "kernels_ms_per_layer": {
             "cues": prof["cues_ms"] / max(1, prof["calls"]),
             "retention": prof["select_ms"] / max(1, prof["calls"]),

@@ -98,7 +98,8 @@ _SIGS = {
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p]),
-    "evisel_profile_begin": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32]),
+    "evisel_profile_begin": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32]),
     "evisel_profile_end": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]),
     "evisel_last_error": (ctypes.c_char_p, []),
@@ -346,11 +347,13 @@ def frame_evidence(mask: Mask, evidence, n_layers: int, e_qf,
         _stream(stream)))
 
 
-def profile_begin(capacity: int, all_kernels: bool = True):
-    """Start timing the kernels of the next ``capacity`` prefill calls
+def profile_begin(capacity: int, all_kernels: bool = True, stride: int = 1):
+    """Start timing the kernels of up to ``capacity`` of the following
+    prefill calls: calls 0, stride, 2*stride, ... of the session
     (``all_kernels`` False: the attention kernel only, so that the others
     run back to back)."""
-    _check(load().evisel_profile_begin(int(capacity), int(bool(all_kernels))))
+    _check(load().evisel_profile_begin(int(capacity), int(bool(all_kernels)),
+                                       int(stride)))
 
 
 def profile_end() -> dict:

@@ -261,6 +261,8 @@ struct Profile {
   bool all = true;             // every kernel, else the attention kernel only
   std::vector<hipEvent_t> ev;  // kProfEvents per timed call
   size_t used = 0;             // calls recorded
+  int64_t seen = 0;            // prefill calls since the session began
+  int32_t stride = 1;          // calls seen % stride == 0 are recorded
 };
 Profile g_prof;
 constexpr int kProfEvents = 6;
@@ -450,8 +452,8 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
   c.segv = frame_pairs ? w.segv : nullptr;
   c.lse2v = cues ? w.lse2v : nullptr;
   hipStream_t s = (hipStream_t)stream;
-  const bool prof =
-      g_prof.open && g_prof.used < g_prof.ev.size() / kProfEvents;
+  const bool prof = g_prof.open && g_prof.seen++ % g_prof.stride == 0 &&
+                    g_prof.used < g_prof.ev.size() / kProfEvents;
   const size_t call = g_prof.used;
   if (prof) prof_record(call, 0, s);
   hipError_t e = hipSuccess;
@@ -601,12 +603,15 @@ evisel_status evisel_frame_evidence(const evisel_mask* m,
   return EVISEL_OK;
 }
 
-evisel_status evisel_profile_begin(int32_t capacity, int32_t all_kernels) {
+evisel_status evisel_profile_begin(int32_t capacity, int32_t all_kernels,
+                                   int32_t stride) {
   if (capacity < 1) return fail(EVISEL_ERR_INVALID_ARG, "capacity < 1");
+  if (stride < 1) return fail(EVISEL_ERR_INVALID_ARG, "stride < 1");
   if (g_prof.open)
     return fail(EVISEL_ERR_INVALID_ARG, "a profiling session is open");
   g_prof = Profile();
   g_prof.all = all_kernels != 0;
+  g_prof.stride = stride;
   try {
     g_prof.ev.resize((size_t)capacity * kProfEvents);
   } catch (const std::bad_alloc&) {

@@ -212,9 +212,17 @@ def test_deterministic_bitwise():
 
 def test_profile_sessions():
     """Kernel timing: with all_kernels the five spans are recorded; without,
-    only the attention kernel's, and the others read 0."""
+    only the attention kernel's, and the others read 0. With a stride, only
+    calls 0, stride, ... of the session are timed, up to the capacity."""
     w = wl.get(2)
     say("case profile sessions")
+    for stride, capacity, n_calls, timed in ((2, 4, 5, 3), (1, 2, 3, 2)):
+        pytest.ev.profile_begin(capacity, all_kernels=False, stride=stride)
+        try:
+            run_gpu(pytest.ev, w, [0] * n_calls, keep_o=False)
+        finally:
+            prof = pytest.ev.profile_end()
+        assert prof["calls"] == timed and prof["attention_ms"] > 0
     for all_kernels in (False, True):
         pytest.ev.profile_begin(4, all_kernels=all_kernels)
         try:

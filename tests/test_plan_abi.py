@@ -272,5 +272,6 @@ def test_error_codes(lib):
     assert st == ev.ERR_INVALID_ARG
     lib.evisel_mask_free(None)                   # ignored
     # kernel-timing sessions: argument errors come before any HIP call
-    assert lib.evisel_profile_begin(0, 0) == ev.ERR_INVALID_ARG
+    assert lib.evisel_profile_begin(0, 0, 1) == ev.ERR_INVALID_ARG
+    assert lib.evisel_profile_begin(4, 0, 0) == ev.ERR_INVALID_ARG
     assert lib.evisel_profile_end(None, None) == ev.ERR_INVALID_ARG
