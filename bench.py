@@ -309,8 +309,14 @@ def main():
         flop_layer = tile_flop * w.hq * st["n_active_pairs"]
     attn_ms = prof_attn["attention_ms"] / max(1, prof_attn["calls"])
     achieved = flop_layer / (attn_ms * 1e-3) / 1e12
-    ev_ms = prof["evidence_ms"] / max(1, prof["calls"])
-    ev_bytes = 4.0 * w.hq * (st["n_text_rows"] * T + st["n_text_rows"] + T)
+    # combine + evidence kernel: the query rows' per-frame partial masses
+    # and the evidence row, the chunk partials (O, reference max, row sum,
+    # non-visual mass), the merged O and LSE of the query rows
+    ev_ms = prof["combine_ms"] / max(1, prof["calls"])
+    segtot = int(np.sum(np.asarray(nt, np.int64) * np.asarray(nf, np.int64)))
+    ev_bytes = (4.0 * w.hq * (segtot + T)
+                + st["n_chunk_slots"] * 64.0 * (4 * w.d + 12)
+                + st["n_text_rows"] * w.hq * (2.0 * w.d + 4))
     rec = {
         "metric": "probe prefill tokens/sec + active-block attention TFLOP/s "
                   "(% bf16 MFMA peak)",
@@ -345,8 +351,7 @@ def main():
             "cues": prof["cues_ms"] / max(1, prof["calls"]),
             "retention": prof["select_ms"] / max(1, prof["calls"]),
             "attention": attn_ms,
-            "combine": prof["combine_ms"] / max(1, prof["calls"]),
-            "evidence": ev_ms},
+            "combine_evidence": ev_ms},
         "evidence_reduce_GBps": ev_bytes / (ev_ms * 1e-3) / 1e9,
         **({"cues": cue_record(w, st, S, T, prof)} if args.cues else {}),
         "topk_planted_recovered": planted_ok,

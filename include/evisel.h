@@ -301,23 +301,24 @@ evisel_status evisel_frame_evidence(const evisel_mask* mask,
                                     const float* frame_pairs, float* e_ff,
                                     void* stream);
 
-/* Kernel timing, a tracing aid. evisel_profile_begin creates 6 * capacity
+/* Kernel timing, a tracing aid. evisel_profile_begin creates 5 * capacity
  * HIP events on the current device. The evisel_sparse_prefill calls that
  * follow are counted from 0; calls 0, stride, 2 * stride, ... are timed, up
  * to `capacity` timed calls, and the others record nothing. With
  * all_kernels != 0 a timed call records events on its stream before the
  * top-p retention (empty for a static mask), before the attention kernel,
- * after it, after the split-row combine, after the evidence reduction and
- * after the frame cues (empty when none is requested). With all_kernels == 0
- * it records only the two events around the attention kernel, so that the
- * other kernels run back to back. Each event is a dependency packet that
- * leaves the GPU idle for several microseconds, hence the stride.
- * evisel_profile_end waits for those events, writes the summed milliseconds
- * of the five spans into ms[0..4] (retention, attention, combine, evidence,
- * cues; spans that were not recorded are 0) and the number of timed calls
- * (either pointer may be NULL) and destroys the events. One session at a
- * time per process; not thread-safe. Errors: INVALID_ARG (capacity < 1,
- * stride < 1, a session already open or none open), NOMEM, HIP. */
+ * after it, after the kernel that merges the split query rows and reduces
+ * the evidence, and after the frame cues (empty when none is requested).
+ * With all_kernels == 0 it records only the two events around the attention
+ * kernel, so that the other kernels run back to back. Each event is a
+ * dependency packet that leaves the GPU idle for several microseconds,
+ * hence the stride. evisel_profile_end waits for those events, writes the
+ * summed milliseconds of the four spans into ms[0..3] (retention,
+ * attention, combine and evidence, cues; spans that were not recorded are
+ * 0) and the number of timed calls (either pointer may be NULL) and
+ * destroys the events. One session at a time per process; not thread-safe.
+ * Errors: INVALID_ARG (capacity < 1, stride < 1, a session already open or
+ * none open), NOMEM, HIP. */
 evisel_status evisel_profile_begin(int32_t capacity, int32_t all_kernels,
                                    int32_t stride);
 evisel_status evisel_profile_end(double* ms, int64_t* n_calls);

@@ -358,8 +358,8 @@ def profile_begin(capacity: int, all_kernels: bool = True, stride: int = 1):
 
 def profile_end() -> dict:
     """Finish the timing session: summed ms per kernel and the call count."""
-    ms = (ctypes.c_double * 5)()
+    ms = (ctypes.c_double * 4)()
     n = ctypes.c_int64()
     _check(load().evisel_profile_end(ms, ctypes.byref(n)))
     return {"select_ms": ms[0], "attention_ms": ms[1], "combine_ms": ms[2],
-            "evidence_ms": ms[3], "cues_ms": ms[4], "calls": n.value}
+            "cues_ms": ms[3], "calls": n.value}

@@ -151,8 +151,7 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
 }
 
 struct WsLayout {
-  size_t pO, pM, pL, pNV, seg, lse2t, tmpart, kbar, rbits, ubits, cpart,
-      total;
+  size_t pO, pM, pL, pNV, seg, kbar, rbits, ubits, cpart, total;
   size_t segv, lse2v, intra_part, cue_total;   // frame cues, after `total`
 };
 
@@ -170,8 +169,6 @@ WsLayout ws_layout(const evisel::Plan& P, int32_t d) {
   w.pL = take(rows * 4);
   w.pNV = take(rows * 4);
   w.seg = take((size_t)P.hq * P.segtot * 4);
-  w.lse2t = take((size_t)P.hq * P.n_text_rows * 4);
-  w.tmpart = take((size_t)P.hq * P.tiles.size() * 4);
   if (P.rule.tau > 0.f) {
     const size_t nb = P.blocks.size();
     // bf16 keeps hi and lo (2 x 2 bytes), fp32 one float: 4 bytes either way
@@ -204,8 +201,6 @@ evisel::Workspace carve(const WsLayout& wl, void* workspace, bool topp,
   w.pL = (float*)(wb + wl.pL);
   w.pNV = (float*)(wb + wl.pNV);
   w.seg = (float*)(wb + wl.seg);
-  w.lse2t = (float*)(wb + wl.lse2t);
-  w.tmpart = (float*)(wb + wl.tmpart);
   w.kbar = topp ? (void*)(wb + wl.kbar) : nullptr;
   w.rbits = topp ? (uint32_t*)(wb + wl.rbits) : nullptr;
   w.ubits = topp ? (uint32_t*)(wb + wl.ubits) : nullptr;
@@ -265,7 +260,7 @@ struct Profile {
   int32_t stride = 1;          // calls seen % stride == 0 are recorded
 };
 Profile g_prof;
-constexpr int kProfEvents = 6;
+constexpr int kProfEvents = 5;
 constexpr int kProfAttn = 1;   // events kProfAttn, kProfAttn + 1 bracket K1
 
 void prof_record(size_t call, int k, hipStream_t s) {
@@ -470,15 +465,12 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
   e = evisel::launch_attention(m->dp, w, c, s);
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   if (prof) prof_record(call, 2, s);
-  e = evisel::launch_combine(m->dp, w, c, s);
-  if (e != hipSuccess) return hip_fail(e, "combine launch");
-  if (prof) prof_record(call, 3, s);
-  e = evisel::launch_evidence(
-      m->dp, w, evidence + (size_t)layer * P.hq * P.T,
+  e = evisel::launch_combine_evidence(
+      m->dp, w, c, evidence + (size_t)layer * P.hq * P.T,
       text_mass ? text_mass + (size_t)layer * P.hq * P.seqs.size() : nullptr,
       s);
-  if (e != hipSuccess) return hip_fail(e, "evidence launch");
-  if (prof) prof_record(call, 4, s);
+  if (e != hipSuccess) return hip_fail(e, "combine and evidence launch");
+  if (prof) prof_record(call, 3, s);
   if (frame_pairs) {
     e = evisel::launch_frame_pairs(
         m->dp, w, frame_pairs + (size_t)layer * P.pairs.size(), s);
@@ -491,7 +483,7 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
     if (e != hipSuccess) return hip_fail(e, "intra-frame launch");
   }
   if (prof) {
-    prof_record(call, 5, s);
+    prof_record(call, 4, s);
     g_prof.used++;
   }
   return EVISEL_OK;

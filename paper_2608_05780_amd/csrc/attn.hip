@@ -1,5 +1,5 @@
 // Block-sparse prefill attention for gfx950 with fused query-frame evidence
-// partials, and the combine step of split query-token rows.
+// partials.
 //
 // Work item = one query block (a region block of <= 64 tokens), up to two
 // query heads sharing one kv head, and a run of the block's active key
@@ -55,7 +55,8 @@
 // Visual and system rows finish in the kernel (O, LSE). Query-token rows are
 // split into chunks of key blocks (longest-first balance across the chip);
 // each chunk leaves an unnormalised partial (acc, m_ref, row sum, non-visual
-// mass) in the workspace and the combine kernel merges them.
+// mass) in the workspace, and the combine part of combine_evidence_kernel
+// merges them.
 #include <algorithm>
 
 #include "kernels.h"
@@ -925,76 +926,6 @@ __global__ __launch_bounds__(256) void intra_reduce_kernel(
   }
 }
 
-// ---------------------------------------------------------------------------
-// Merge the chunks of a query-token tile: one work-group per (tile, head),
-// eight threads per row. Also leaves the rows' log2 LSE for the evidence
-// reduction and the tile's non-visual mass.
-constexpr int kCombineThreads = 512;
-
-template <int D, bool F32>
-__global__ __launch_bounds__(kCombineThreads) void combine_kernel(
-    const DevPlan pl, const Workspace ws, const AttnCall ac) {
-  constexpr int DP = D / 8;
-  __shared__ float red[kTile];
-  const TextTile tt = pl.tiles[blockIdx.x];
-  const int h = blockIdx.y;
-  const BlockDesc qb = pl.blocks[tt.qblock];
-  const int tid = threadIdx.x, r = tid >> 3, part = tid & 7;
-  float nvmass = 0.f;
-  if (r < qb.len) {
-    const int slot0 = tt.slot0 + h * tt.n_chunks;
-    float M = neg_inf();
-    for (int c = 0; c < tt.n_chunks; ++c)
-      M = fmaxf(M, ws.pM[(size_t)(slot0 + c) * kTile + r]);
-    float L = 0.f;
-    float acc[DP];
-#pragma unroll
-    for (int i = 0; i < DP; ++i) acc[i] = 0.f;
-    for (int c = 0; c < tt.n_chunks; ++c) {
-      const size_t ix = (size_t)(slot0 + c) * kTile + r;
-      const float m = ws.pM[ix];
-      const float w = m == neg_inf() ? 0.f : exp2_(m - M);
-      L += w * ws.pL[ix];
-      const float* po = ws.pO + ix * D + part * DP;
-#pragma unroll
-      for (int i = 0; i < DP; i += 4) {
-        const f32x4 t = *(const f32x4*)(po + i);
-        acc[i] += w * t[0];
-        acc[i + 1] += w * t[1];
-        acc[i + 2] += w * t[2];
-        acc[i + 3] += w * t[3];
-      }
-    }
-    const float inv = 1.f / L;
-    const int qpos = qb.start + r;
-#pragma unroll
-    for (int i = 0; i < DP; i += 4) {
-      f32x4 v = {acc[i] * inv, acc[i + 1] * inv, acc[i + 2] * inv,
-                 acc[i + 3] * inv};
-      const size_t off = ((size_t)qpos * pl.hq + h) * D + part * DP + i;
-      if (F32) {
-        *(f32x4*)((float*)ac.o + off) = v;
-      } else {
-        *(bf16x4*)((__bf16*)ac.o + off) = __builtin_convertvector(v, bf16x4);
-      }
-    }
-    const float lse2 = M + log2_(L);
-    if (part == 0) {
-      if (ac.lse) ac.lse[(size_t)h * pl.S + qpos] = lse2 * kLn2;
-      ws.lse2t[(size_t)h * pl.n_text_rows + qb.aux + r] = lse2;
-      for (int c = 0; c < tt.n_chunks; ++c)
-        nvmass += exp2_(ws.pNV[(size_t)(slot0 + c) * kTile + r] - lse2);
-    }
-  }
-  if (part == 0) red[r] = nvmass;
-  __syncthreads();
-  if (tid == 0) {
-    float t = 0.f;
-    for (int i = 0; i < kTile; ++i) t += red[i];
-    ws.tmpart[(size_t)h * pl.n_tiles + blockIdx.x] = t;
-  }
-}
-
 }  // namespace
 
 hipError_t launch_attention(const DevPlan& p, const Workspace& w,
@@ -1049,24 +980,6 @@ hipError_t launch_intra_frame(const DevPlan& p, const Workspace& w,
   const size_t n = (size_t)p.T * p.Nv * p.Nv;
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
   intra_reduce_kernel<<<dim3(blocks), dim3(256), 0, s>>>(p, w, out);
-  return hipGetLastError();
-}
-
-hipError_t launch_combine(const DevPlan& p, const Workspace& w,
-                          const AttnCall& c, hipStream_t s) {
-  if (p.n_tiles == 0) return hipSuccess;
-  dim3 grid(p.n_tiles, p.hq), block(kCombineThreads);
-  if (c.fp32) {
-    if (c.d == 64)
-      combine_kernel<64, true><<<grid, block, 0, s>>>(p, w, c);
-    else
-      combine_kernel<128, true><<<grid, block, 0, s>>>(p, w, c);
-  } else {
-    if (c.d == 64)
-      combine_kernel<64, false><<<grid, block, 0, s>>>(p, w, c);
-    else
-      combine_kernel<128, false><<<grid, block, 0, s>>>(p, w, c);
-  }
   return hipGetLastError();
 }
 

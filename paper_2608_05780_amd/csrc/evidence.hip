@@ -1,12 +1,26 @@
-// Evidence reduction and frame aggregation (gfx950).
+// Query-row merge, evidence reduction and frame aggregation (gfx950).
 //
-// evidence_kernel: E[h, f] = sum over the query rows r of f's video of
-//   exp2(seg[h, r, f] - lse2[h, r]), i.e. each row's softmax mass on frame f
-//   (the query-frame cue of Evidence Decomposition, kept as a raw sum over the
-//   query rows). A work-group takes 64 frames of one head; 16 row groups sum
-//   strided rows and are added in a fixed order in LDS, one store per
-//   output: no atomics, bitwise reproducible. Adjacent threads read adjacent
-//   frames of the same row, so every load is coalesced.
+// combine_evidence_kernel: one launch, three independent parts (ranges of
+//   the block index), so that no part waits for another:
+//   combine    one work-group per (query-token tile, head): merges the
+//              tile's chunk partials into O and the LSE, sixteen threads per
+//              row (each a contiguous D/16 slice);
+//   evidence   one work-group per (64 frames, head): E[h, f] = sum over the
+//              query rows r of f's video of exp2(seg[h, r, f] - lse2[h, r]),
+//              i.e. each row's softmax mass on frame f (the query-frame cue
+//              of Evidence Decomposition, kept as a raw sum over the query
+//              rows). 16 row groups sum strided rows and are added in a fixed
+//              order in LDS, one store per output: no atomics, bitwise
+//              reproducible. Adjacent threads read adjacent frames of the
+//              same row, so every load is coalesced;
+//   text mass  one work-group per (head, video), only when requested: the
+//              video's query-row mass on non-visual keys (system prefix and
+//              query tokens); one wavefront per tile, rows and then tiles
+//              added in a fixed order.
+//   Every part that needs a row's log2 LSE rebuilds it from the chunk
+//   partials the same way: the largest chunk reference, then the rescaled
+//   chunk row sums added in chunk order. The evidence part computes the
+//   LSE of the rows its frames read once into LDS (when they fit).
 // frame_mean_kernel: E_qf[l, t] = sum_h E[l, h, t] / (Hq * n_text) and the
 //   mean over layers (heads averaged per layer, layer kept); 32 frames x 32
 //   layer groups per work-group, layers added in a fixed order.
@@ -18,45 +32,189 @@
 namespace evisel {
 namespace {
 
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kTile = 64;
+constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 __device__ __forceinline__ float exp2_(float x) {
   return __builtin_amdgcn_exp2f(x);
 }
+__device__ __forceinline__ float log2_(float x) {
+  return __builtin_amdgcn_logf(x);
+}
 
-constexpr int kEvFrames = 64, kEvRows = 16;
-
-__global__ __launch_bounds__(kEvFrames * kEvRows) void evidence_kernel(
-    const DevPlan pl, const Workspace ws, float* __restrict__ ev,
-    float* __restrict__ tm) {
-  __shared__ float red[kEvRows][kEvFrames];
-  const int h = blockIdx.y;
-  const int fl = threadIdx.x % kEvFrames, rg = threadIdx.x / kEvFrames;
-  const int f = blockIdx.x * kEvFrames + fl;
-  float acc = 0.f;
-  if (f < pl.T) {
-    const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
-    const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
-                       (f - sq.frame0);
-    const float* l2 = ws.lse2t + (size_t)h * pl.n_text_rows + sq.textrow0;
-#pragma unroll 4
-    for (int r = rg; r < sq.n_text; r += kEvRows)
-      acc += exp2_(src[(size_t)r * sq.n_frames] - l2[r]);
+// log2 LSE of row r of a query-token tile from its chunk partials (chunk
+// slots slot0 .. slot0 + nch - 1).
+__device__ __forceinline__ float row_lse2(const Workspace& ws, int slot0,
+                                          int nch, int r) {
+  float M = neg_inf();
+  for (int c = 0; c < nch; ++c)
+    M = fmaxf(M, ws.pM[(size_t)(slot0 + c) * kTile + r]);
+  float L = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const size_t ix = (size_t)(slot0 + c) * kTile + r;
+    const float m = ws.pM[ix];
+    const float w = m == neg_inf() ? 0.f : exp2_(m - M);
+    L += w * ws.pL[ix];
   }
-  red[rg][fl] = acc;
-  __syncthreads();
-  if (rg == 0 && f < pl.T) {
-    float t = 0.f;
+  return M + log2_(L);
+}
+
+// Sum over the 64 lanes of a wavefront, in a fixed butterfly order (the
+// same result on every lane, reproducible run to run).
+__device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
-    for (int i = 0; i < kEvRows; ++i) t += red[i][fl];
-    ev[(size_t)h * pl.T + f] = t;
-  }
-  if (tm && blockIdx.x == 0) {
-    for (int n = threadIdx.x; n < pl.n_seq; n += kEvFrames * kEvRows) {
-      const SeqDesc sq = pl.seqs[n];
-      float t = 0.f;
-      for (int i = 0; i < sq.n_tiles; ++i)
-        t += ws.tmpart[(size_t)h * pl.n_tiles + sq.tile0 + i];
-      tm[(size_t)h * pl.n_seq + n] = t;
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// Row `rr` (0-based) of video sq's query tokens, head h.
+__device__ __forceinline__ float text_row_lse2(const DevPlan& pl,
+                                               const Workspace& ws,
+                                               const SeqDesc& sq, int h,
+                                               int rr) {
+  const TextTile tt = pl.tiles[sq.tile0 + (rr >> 6)];
+  return row_lse2(ws, tt.slot0 + h * tt.n_chunks, tt.n_chunks, rr & 63);
+}
+
+constexpr int kCeThreads = 1024;
+constexpr int kEvFrames = 64, kEvRows = kCeThreads / kEvFrames;   // 16
+constexpr int kLseCache = 4096;   // query rows whose LSE the evidence part
+                                  // keeps in LDS
+
+template <int D, bool F32>
+__global__ __launch_bounds__(kCeThreads) void combine_evidence_kernel(
+    const DevPlan pl, const Workspace ws, const AttnCall ac,
+    float* __restrict__ ev, float* __restrict__ tm) {
+  __shared__ float red[kEvRows][kEvFrames];
+  __shared__ float l2c[kLseCache];
+  const int tid = threadIdx.x;
+  const int n_comb = pl.n_tiles * pl.hq;
+  const int n_fb = (pl.T + kEvFrames - 1) / kEvFrames;
+  int bid = blockIdx.x;
+
+  if (bid < n_comb) {
+    // ---- combine: tile bid % n_tiles, head bid / n_tiles
+    constexpr int DP = D / 16;
+    const TextTile tt = pl.tiles[bid % pl.n_tiles];
+    const int h = bid / pl.n_tiles;
+    const BlockDesc qb = pl.blocks[tt.qblock];
+    const int r = tid >> 4, part = tid & 15;
+    if (r >= qb.len) return;
+    const int slot0 = tt.slot0 + h * tt.n_chunks;
+    float M = neg_inf();
+    for (int c = 0; c < tt.n_chunks; ++c)
+      M = fmaxf(M, ws.pM[(size_t)(slot0 + c) * kTile + r]);
+    float L = 0.f;
+    float acc[DP];
+#pragma unroll
+    for (int i = 0; i < DP; ++i) acc[i] = 0.f;
+    for (int c = 0; c < tt.n_chunks; ++c) {
+      const size_t ix = (size_t)(slot0 + c) * kTile + r;
+      const float m = ws.pM[ix];
+      const float w = m == neg_inf() ? 0.f : exp2_(m - M);
+      L += w * ws.pL[ix];
+      const float* po = ws.pO + ix * D + part * DP;
+#pragma unroll
+      for (int i = 0; i < DP; i += 4) {
+        const f32x4 t = *(const f32x4*)(po + i);
+        acc[i] += w * t[0];
+        acc[i + 1] += w * t[1];
+        acc[i + 2] += w * t[2];
+        acc[i + 3] += w * t[3];
+      }
     }
+    const float inv = 1.f / L;
+    const int qpos = qb.start + r;
+#pragma unroll
+    for (int i = 0; i < DP; i += 4) {
+      const f32x4 v = {acc[i] * inv, acc[i + 1] * inv, acc[i + 2] * inv,
+                       acc[i + 3] * inv};
+      const size_t off = ((size_t)qpos * pl.hq + h) * D + part * DP + i;
+      if (F32)
+        *(f32x4*)((float*)ac.o + off) = v;
+      else
+        *(bf16x4*)((__bf16*)ac.o + off) = __builtin_convertvector(v, bf16x4);
+    }
+    if (part == 0 && ac.lse)
+      ac.lse[(size_t)h * pl.S + qpos] = (M + log2_(L)) * kLn2;
+    return;
+  }
+  bid -= n_comb;
+
+  if (bid < n_fb * pl.hq) {
+    // ---- evidence: frames [f0, f0 + 64) of head h
+    const int h = bid / n_fb, f0 = (bid % n_fb) * kEvFrames;
+    const int fl = tid % kEvFrames, rg = tid / kEvFrames;
+    const int f = f0 + fl;
+    // the query rows of the videos these frames belong to are consecutive
+    const SeqDesc s0 = pl.seqs[pl.frame_seq[f0]];
+    const SeqDesc s1 = pl.seqs[pl.frame_seq[min(f0 + kEvFrames, pl.T) - 1]];
+    const int r0 = s0.textrow0, nrows = s1.textrow0 + s1.n_text - r0;
+    const bool cached = nrows <= kLseCache;
+    if (cached) {
+      for (int n = pl.frame_seq[f0]; n <= pl.frame_seq[min(f0 + kEvFrames,
+                                                           pl.T) - 1]; ++n) {
+        const SeqDesc sq = pl.seqs[n];
+        for (int rr = tid; rr < sq.n_text; rr += kCeThreads)
+          l2c[sq.textrow0 - r0 + rr] = text_row_lse2(pl, ws, sq, h, rr);
+      }
+      __syncthreads();
+    }
+    float acc = 0.f;
+    if (f < pl.T) {
+      const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
+      const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
+                         (f - sq.frame0);
+      const float* l2 = l2c + (sq.textrow0 - r0);
+      if (cached) {
+#pragma unroll 4
+        for (int r = rg; r < sq.n_text; r += kEvRows)
+          acc += exp2_(src[(size_t)r * sq.n_frames] - l2[r]);
+      } else {
+        for (int r = rg; r < sq.n_text; r += kEvRows)
+          acc += exp2_(src[(size_t)r * sq.n_frames] -
+                       text_row_lse2(pl, ws, sq, h, r));
+      }
+    }
+    red[rg][fl] = acc;
+    __syncthreads();
+    if (rg == 0 && f < pl.T) {
+      float t = 0.f;
+#pragma unroll
+      for (int i = 0; i < kEvRows; ++i) t += red[i][fl];
+      ev[(size_t)h * pl.T + f] = t;
+    }
+    return;
+  }
+  bid -= n_fb * pl.hq;
+
+  // ---- text mass of (head, video): wave w takes the video's tiles w,
+  // w + 16, ...; lane = row of the tile
+  const int h = bid / pl.n_seq, n = bid % pl.n_seq;
+  const SeqDesc sq = pl.seqs[n];
+  const int lane = tid & 63, wave = tid >> 6;
+  float wsum = 0.f;
+  for (int i = wave; i < sq.n_tiles; i += kCeThreads / 64) {
+    const TextTile tt = pl.tiles[sq.tile0 + i];
+    float nv = 0.f;
+    if (lane < pl.blocks[tt.qblock].len) {
+      const int slot0 = tt.slot0 + h * tt.n_chunks;
+      const float l2 = row_lse2(ws, slot0, tt.n_chunks, lane);
+      for (int c = 0; c < tt.n_chunks; ++c)
+        nv += exp2_(ws.pNV[(size_t)(slot0 + c) * kTile + lane] - l2);
+    }
+    wsum += wave_sum(nv);
+  }
+  float* part = &red[0][0];
+  if (lane == 0) part[wave] = wsum;
+  __syncthreads();
+  if (wave == 0) {
+    const float t = wave_sum(lane < kCeThreads / 64 ? part[lane] : 0.f);
+    if (lane == 0) tm[(size_t)h * pl.n_seq + n] = t;
   }
 }
 
@@ -232,11 +390,27 @@ hipError_t launch_e_ff(const DevPlan& p, const float* pairs,
   return hipGetLastError();
 }
 
-hipError_t launch_evidence(const DevPlan& p, const Workspace& w, float* ev,
-                           float* tm, hipStream_t s) {
-  dim3 grid((p.T + kEvFrames - 1) / kEvFrames, p.hq),
-      block(kEvFrames * kEvRows);
-  evidence_kernel<<<grid, block, 0, s>>>(p, w, ev, tm);
+hipError_t launch_combine_evidence(const DevPlan& p, const Workspace& w,
+                                   const AttnCall& c, float* ev, float* tm,
+                                   hipStream_t s) {
+  const int n_fb = (p.T + kEvFrames - 1) / kEvFrames;
+  const int blocks =
+      p.n_tiles * p.hq + n_fb * p.hq + (tm ? p.hq * p.n_seq : 0);
+  dim3 grid(blocks), block(kCeThreads);
+  if (c.fp32) {
+    if (c.d == 64)
+      combine_evidence_kernel<64, true><<<grid, block, 0, s>>>(p, w, c, ev, tm);
+    else
+      combine_evidence_kernel<128, true><<<grid, block, 0, s>>>(p, w, c, ev,
+                                                                tm);
+  } else {
+    if (c.d == 64)
+      combine_evidence_kernel<64, false><<<grid, block, 0, s>>>(p, w, c, ev,
+                                                                tm);
+    else
+      combine_evidence_kernel<128, false><<<grid, block, 0, s>>>(p, w, c, ev,
+                                                                 tm);
+  }
   return hipGetLastError();
 }
 

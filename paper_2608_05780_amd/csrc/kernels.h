@@ -42,8 +42,6 @@ struct Workspace {
   float* pL;     // [slots][64]     partial row sums
   float* pNV;    // [slots][64]     log2 partial mass on non-visual keys
   float* seg;    // [hq][segtot]    log2 partial mass per (query row, frame)
-  float* lse2t;  // [hq][n_text_rows] log2 LSE of query rows
-  float* tmpart; // [hq][n_tiles]   non-visual mass per query tile
   // top-p retention (null for the static rule)
   void* kbar;              // bf16: hi [hkv][nb][d] then lo; fp32: [hkv][nb][d]
   uint32_t* rbits;         // [hq][nb][W][64] retained history per row
@@ -99,11 +97,12 @@ hipError_t launch_coarse(const DevPlan& p, const Workspace& w,
 // of a work item retained are skipped and leave no partial).
 hipError_t launch_seg_fill(const DevPlan& p, const Workspace& w,
                            hipStream_t s);
-hipError_t launch_combine(const DevPlan& p, const Workspace& w,
-                          const AttnCall& c, hipStream_t s);
-hipError_t launch_evidence(const DevPlan& p, const Workspace& w,
-                           float* evidence_layer, float* text_mass_layer,
-                           hipStream_t s);
+// Merge of the split query-token rows (O and LSE into c's outputs), the
+// layer's evidence [hq][T] and, when text_mass_layer is not null, the
+// query rows' non-visual mass [hq][n_seq], in one launch.
+hipError_t launch_combine_evidence(const DevPlan& p, const Workspace& w,
+                                   const AttnCall& c, float* evidence_layer,
+                                   float* text_mass_layer, hipStream_t s);
 hipError_t launch_frame_evidence(const DevPlan& p, const float* evidence,
                                  int32_t n_layers, float* e_qf_layer,
                                  float* e_qf, const int32_t* k_per_seq,
