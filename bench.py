@@ -72,17 +72,42 @@ def measured_traffic():
     return None
 
 
+def work_units(ev, mask):
+    """The attention work list as (query block, first head, heads, CSR run)
+    units: an ordinary item is one unit; a paired item (one head over two
+    query blocks) is one unit per query block, its run read back from the
+    paired-tile list."""
+    import numpy as np
+    wk = ev.mask_export_work(mask)
+    pt = ev.mask_export_paired(mask)
+    units = []
+    for qb, h0, nh, a, e, q2 in zip(wk["qblock"], wk["head"], wk["nheads"],
+                                    wk["kb_begin"], wk["kb_end"],
+                                    wk["qblock2"]):
+        if qb < 0:
+            continue
+        if q2 < 0:
+            units.append((int(qb), int(h0), int(nh), int(a), int(e)))
+            continue
+        for q, pos in ((qb, pt["pos_a"][a:e]), (q2, pt["pos_b"][a:e])):
+            p = pos[pos >= 0]
+            units.append((int(q), int(h0), 1, int(p[0]), int(p[-1]) + 1))
+    return units
+
+
 def topp_computed_pairs(ev, mask, w, qs, kks, ws):
     """Key tiles the top-p attention computes per layer (mean over
     layers), summed over query heads, and the mean fraction of its history
-    a row retains. Recomputes each layer's retention (same kernels)."""
+    a row retains. Recomputes each layer's retention (same kernels). A unit
+    of work computes a candidate tile when it is always visible or some row
+    of the unit's heads retained it."""
     import numpy as np
     import torch
     st = mask.stats
     nb, W = st["n_blocks"], st["hist_words"]
     ex = ev.mask_export(mask)
-    wk = ev.mask_export_work(mask)
-    col, rp = ex["col"], ex["row_ptr"]
+    units = work_units(ev, mask)
+    col = ex["col"]
     # local history index of every block (-1: system prefix)
     local = np.full(nb, -1, np.int64)
     for n in np.unique(ex["video"]):
@@ -95,10 +120,7 @@ def topp_computed_pairs(ev, mask, w, qs, kks, ws):
         ev.select_blocks(mask, qs[l], kks[l], rb, ub, ws,
                          softmax_scale=w.softmax_scale)
         u = ub.cpu().numpy().view(np.uint32)
-        for qb, h0, nh, a, e in zip(wk["qblock"], wk["head"], wk["nheads"],
-                                    wk["kb_begin"], wk["kb_end"]):
-            if qb < 0:
-                continue
+        for qb, h0, nh, a, e in units:
             c = col[a:e]
             loc = local[c]
             always = (loc < 0) | (c == qb)

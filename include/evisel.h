@@ -145,8 +145,8 @@ evisel_status evisel_mask_export(const evisel_mask* mask, int32_t* blk_start,
  * (consecutive, sharing one kv head), first and one-past-last CSR position
  * of its key blocks, and the first head's split slot (-1 unless the item is
  * part of a split query-token row). Any pointer may be NULL.
- * With the static rule and an odd number of query heads per kv head, the
- * odd head of a kv group is covered by paired items: one head over two
+ * With an odd number of query heads per kv head, the odd head of a kv
+ * group is covered by paired items: one head over two
  * query blocks of the same video and region (qblock and qblock2 >= 0; for
  * split query-token rows, the same chunk of two consecutive query-token
  * blocks, with slots slot and slot2). A paired item's [kb_begin, kb_end)

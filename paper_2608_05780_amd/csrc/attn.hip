@@ -476,7 +476,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const int hsub = wave >> 1;
   // A paired item gives the second half of the work-group its own query
   // block (same head); otherwise the halves take heads head, head + 1.
-  const bool uni = !TOPP && it.qblock2 >= 0;
+  const bool uni = it.qblock2 >= 0;
   const int nhalf = uni ? 2 : it.nheads;   // halves with rows
   const bool active = hsub < nhalf;
   const int hd1 = uni ? it.head : it.head + 1;   // the second half's head
@@ -485,6 +485,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   const BlockDesc qb0 = pl.blocks[it.qblock];
   const BlockDesc qb1 = uni ? pl.blocks[it.qblock2] : qb0;
   const BlockDesc qb = hsub ? qb1 : qb0;
+  const int qbid = uni && hsub ? it.qblock2 : it.qblock;   // the wave's block
   const bool is_text = it.slot >= 0;
   const int qrow = 32 * (wave & 1) + l32;
   const bool qvalid = active && qrow < qb.len;
@@ -529,16 +530,29 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     if (t < n) {
       const int pos = TOPP ? (int)clist[t] : t;
       const BlockDesc bd =
-          uni ? pl.ptile_desc[b0 + t] : pl.col_desc[b0 + pos];
-      dsc_pos = uni ? pl.ptile[b0 + t].pos[hsub] : b0 + pos;
+          uni ? pl.ptile_desc[b0 + pos] : pl.col_desc[b0 + pos];
       dsc_start = bd.start;
       dsc_len = bd.len;
       dsc_region = bd.region;
       dsc_aux = bd.aux;
-      if (TOPP) {
-        const int bid = pl.col[b0 + pos];
-        const int loc = pl.blk_local[bid];
-        dsc_loc = bid == it.qblock ? -1 : loc;
+      if (uni) {
+        const PairedTile pt = pl.ptile[b0 + pos];
+        dsc_pos = pt.pos[hsub];
+        if (TOPP) {
+          // top-p: a history block no row of this half retained is skipped
+          const int loc = pl.blk_local[pt.block];
+          dsc_loc = pt.block == qbid ? -1 : loc;
+          if (dsc_pos >= 0 && dsc_loc >= 0 &&
+              !((ws.ubits[((size_t)it.head * pl.nb + qbid) * pl.W +
+                          (loc >> 5)] >> (loc & 31)) & 1u))
+            dsc_pos = -1;
+        }
+      } else {
+        dsc_pos = b0 + pos;
+        if (TOPP) {
+          const int bid = pl.col[b0 + pos];
+          dsc_loc = bid == it.qblock ? -1 : pl.blk_local[bid];
+        }
       }
     }
   };
@@ -574,7 +588,23 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       for (int c0 = 0; c0 < n; c0 += 64) {
         const int t = c0 + lane;
         bool keep = false;
-        if (t < n) {
+        if (t < n && uni) {
+          // paired item: kept when either half's rows need it
+          const PairedTile pt = pl.ptile[b0 + t];
+          const int loc = pl.blk_local[pt.block];
+          for (int k = 0; k < 2; ++k) {
+            const int own = k ? it.qblock2 : it.qblock;
+            if (pt.pos[k] < 0) continue;
+            if (loc < 0 || pt.block == own) {
+              keep = true;
+            } else {
+              const unsigned wd =
+                  ws.ubits[((size_t)it.head * pl.nb + own) * pl.W +
+                           (loc >> 5)];
+              keep = keep || ((wd >> (loc & 31)) & 1u);
+            }
+          }
+        } else if (t < n) {
           const int bid = pl.col[b0 + t];
           const int loc = pl.blk_local[bid];
           if (loc < 0 || bid == it.qblock) {
@@ -710,7 +740,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   // Top-p: the row's retained-history word of a tile, fetched with the
   // tile's key/value loads.
   const uint32_t* rrow =
-      TOPP ? ws.rbits + ((size_t)h * pl.nb + it.qblock) * pl.W * 64 + qrow
+      TOPP ? ws.rbits + ((size_t)h * pl.nb + qbid) * pl.W * 64 + qrow
            : nullptr;
   auto row_bits = [&](int loc) -> unsigned {
     return loc < 0 ? ~0u : rrow[(size_t)(loc >> 5) * 64];

@@ -200,11 +200,10 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
   const int64_t avg = (total + kTargetSlots - 1) / kTargetSlots;
   P.chunk_blocks = (int32_t)std::max<int64_t>(16, avg);
 
-  // Paired items (static rule only: top-p items select per row against
-  // their own block's history): the kv group's odd head takes two query
-  // blocks in one item. Both CSR rows are in ascending key-block order, so
-  // their runs merge by key block.
-  const bool pair_rows = !topp;
+  // Paired items: the kv group's odd head takes two query blocks in one
+  // item. Both CSR rows are in ascending key-block order, so their runs
+  // merge by key block. (Under top-p each half skips the history blocks its
+  // own rows did not retain.)
   auto paired = [&](int32_t qa, int32_t a0, int32_t a1, int32_t qb2,
                     int32_t c0, int32_t c1, int32_t h, int32_t slot_a,
                     int32_t slot_b, int32_t n, int32_t nch) {
@@ -251,7 +250,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
         for (int32_t pp = 0; pp < pairs; ++pp) {
           const int32_t h0 = g * group + pp * kHeadsPerItem;
           const int32_t nh = std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
-          const bool pr = nh == 1 && pair_rows;
+          const bool pr = nh == 1;
           // odd head: chunk c of tiles 2i and 2i+1 share one item
           const int32_t c_first =
               pr && ti % 2 == 1 ? std::min(vt[ti - 1].nch, t.nch) : 0;
@@ -284,7 +283,7 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
             const int32_t h0 = g * group + pp * kHeadsPerItem;
             const int32_t nh =
                 std::min(kHeadsPerItem, group - pp * kHeadsPerItem);
-            if (nh == 1 && pair_rows) {
+            if (nh == 1) {
               // odd head: blocks 2i and 2i+1 of the region share one item
               if (i % 2 == 1) continue;
               if (i + 1 < ids.size()) {
