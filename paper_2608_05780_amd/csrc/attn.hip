@@ -58,6 +58,7 @@
 // mass) in the workspace, and the combine part of combine_evidence_kernel
 // merges them.
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -120,13 +121,15 @@ __device__ __forceinline__ int swz(int row) {
 // assembly so that the compiler does not treat later LDS reads as possibly
 // racing with it (it would otherwise wait for every outstanding load,
 // including the next tile's, before the transposed V reads); every caller
-// waits for vmcnt(0) and a barrier before reading the destination.
+// waits for vmcnt(0) and a barrier before reading the destination. The LDS
+// address passes through readfirstlane: it is wave-uniform, and under SGPR
+// pressure the register allocator would otherwise hand the asm a VGPR.
 __device__ __forceinline__ void lds_dma16(uint32_t lds, const char* gbase,
                                           uint32_t voff) {
   asm volatile(
       "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
       :
-      : "s"(lds), "v"(voff), "s"(gbase)
+      : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(gbase)
       : "memory", "m0");
 }
 
@@ -235,11 +238,26 @@ struct Bf16Path {
   // 32c + 16s + 4g + j/4 (+8 for the second) at column
   // 32mt + 16((lane/16) % 2) + 4(j % 4); lane i then holds V[those 4 keys]
   // at column 32mt + lane % 32.
-  __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
-                            const f32x16 (&p)[2], int lane) {
+  // Per-lane part of the transpose-read address of d-tile mt: the lane's
+  // row offset 4g + j/4 and its swizzled chunk. The chunk of d-tile mt is
+  // (4mt + x) ^ sw with x < 4, i.e. (4mt ^ (sw & ~3)) | (x ^ (sw & 3)), so
+  // the k-step part (32c + 16s rows) is a constant added to these.
+  static constexpr int NMT = D / 32;
+  struct PvOff {
+    int v[NMT];
+  };
+  __device__ static void pv_offsets(PvOff& po, int lane) {
     const int j = lane & 15, q16 = lane >> 4, g = lane >> 5;
     const int sw = swz<kSwzV, RC>(j >> 2);   // row % 4 == j / 4 below
-    constexpr int NMT = D / 32;
+    const int x = 2 * (q16 & 1) + ((j & 3) >> 1);
+#pragma unroll
+    for (int mt = 0; mt < NMT; ++mt) {
+      const int ch = ((4 * mt) ^ (sw & ~3)) | (x ^ (sw & 3));
+      po.v[mt] = ((4 * g + (j >> 2)) * RC + ch) * 16 + 8 * (j & 1);
+    }
+  }
+  __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
+                            const f32x16 (&p)[2], const PvOff& po) {
     bf16x8 va[4][NMT];
     bf16x8 pb[4];
 #pragma unroll
@@ -250,12 +268,9 @@ struct Bf16Path {
                               : __builtin_shufflevector(p[c], p[c], 8, 9, 10,
                                                         11, 12, 13, 14, 15);
       pb[cs] = __builtin_convertvector(pf, bf16x8);
-      const int row = 32 * c + 16 * s + 4 * g + (j >> 2);
 #pragma unroll
       for (int mt = 0; mt < NMT; ++mt) {
-        const int col = 32 * mt + 16 * (q16 & 1) + 4 * (j & 3);
-        const int ch = (col >> 3) ^ sw;
-        const EV_LDS char* a0 = vt + (row * RC + ch) * 16 + 8 * (j & 1);
+        const EV_LDS char* a0 = vt + po.v[mt] + (32 * c + 16 * s) * RC * 16;
         const EV_LDS char* a1 = a0 + 8 * RC * 16;   // row + 8
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (EV_LDS i16x4*)a0);
@@ -418,8 +433,13 @@ struct F32Path {
     }
   }
 
+  struct PvOff {
+    int lane;
+  };
+  __device__ static void pv_offsets(PvOff& po, int lane) { po.lane = lane; }
   __device__ static void pv(f32x16 (&o)[D / 32], const EV_LDS char* vt,
-                            const f32x16 (&p)[2], int lane) {
+                            const f32x16 (&p)[2], const PvOff& po) {
+    const int lane = po.lane;
     const int l32 = lane & 31, g = lane >> 5;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
@@ -505,6 +525,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 
   TileLoader<T, D, kSwzK> kload;
   TileLoader<T, D, VSWZ> vload;
+  typename P::PvOff pvo;
+  P::pv_offsets(pvo, lane);
   kload.init(pl.hkv, wave, lane);
   vload.init(pl.hkv, wave, lane);
   // LDS layout: [K0 | K1 | V0 | V1], tile t in buffers t % 2.
@@ -734,7 +756,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         nv_part += ts;
       }
     }
-    P::pv(o, vt, s, lane);
+    P::pv(o, vt, s, pvo);
   };
 
   // Top-p: the row's retained-history word of a tile, fetched with the
@@ -767,7 +789,15 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     __syncthreads();   // staged Q visible to every wave
     P::load_q_lds(qf, hsub ? vbuf(1) : kbuf(1), qrow, g);
   }
-  for (int j = 0; j < n; ++j) {
+  // Tile j lives in buffer pair j % 2. The loop is unrolled by two so that
+  // each copy addresses fixed buffers: their LDS offsets become instruction
+  // immediates instead of a VALU add per operand read.
+  auto step = [&](int j, auto parity) {
+    constexpr int pb = decltype(parity)::value;
+    EV_LDS char* const kc = kbuf0 + pb * TB;
+    EV_LDS char* const vc = vbuf0 + pb * TB;
+    EV_LDS char* const kn = kbuf0 + (1 - pb) * TB;
+    EV_LDS char* const vn = vbuf0 + (1 - pb) * TB;
     const BlockDesc cur = kb;
     const int lcur = lnext, pcur = pnext;
     if (((j + 1) & 63) == 0 && j + 1 < n) load_batch((j + 1) >> 6);
@@ -776,8 +806,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     __syncthreads();
     if (j + 1 < n) {
       kb = desc(j + 1);
-      kload.issue(kbuf(j + 1), kg, kb.start, kb.len, kvh, wave);
-      vload.issue(vbuf(j + 1), vg, kb.start, kb.len, kvh, wave);
+      kload.issue(kn, kg, kb.start, kb.len, kvh, wave);
+      vload.issue(vn, vg, kb.start, kb.len, kvh, wave);
       if (TOPP) {
         lnext = loc_of(j + 1);
         wnext = row_bits(lnext);
@@ -786,11 +816,15 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     }
     if (active && pcur >= 0) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
-      P::qk(s, kbuf(j), qf, l32, g);
+      P::qk(s, kc, qf, l32, g);
       tile_pre(s, cur, wcur, lcur);
       const float ts = tile_main(s);
-      tile_post(s, cur, ts, vbuf(j), pcur);
+      tile_post(s, cur, ts, vc, pcur);
     }
+  };
+  for (int j = 0; j < n; j += 2) {
+    step(j, std::integral_constant<int, 0>{});
+    if (j + 1 < n) step(j + 1, std::integral_constant<int, 1>{});
   }
   const float l_tot = pair_sum(l_part);
   if (P::kStaged && !is_text) {
