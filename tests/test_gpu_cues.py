@@ -139,6 +139,15 @@ TOPP = {
         window=8, plant="choose", n_frames=(40,), n_text=(48,), n_sys=(3,),
         tau_p=float(np.float32(0.97)), key_struct=(2.0, 2.0, 0.8),
         plant_args={"count": 2, "s_frame": (2.0, 2.0), "s_query": 2.0}),
+    # three query heads per kv head: the odd head's work runs as paired
+    # items, each half computing only the tiles its own rows retained
+    "odd_group_struct": wl.Workload(
+        name="odd-group-struct", config_id=900, n_layers=1, hq=6, hkv=2,
+        d=128, dtype="bf16", tokens_per_frame=32, block=64, sink_blocks=1,
+        window=8, plant="choose", n_frames=(9, 40, 5), n_text=(64, 70, 130),
+        n_sys=(5, 0, 70), n_videos=3, tau_p=0.9,
+        key_struct=(2.0, 2.0, 0.8),
+        plant_args={"count": 2, "s_frame": (2.0, 2.0), "s_query": 2.0}),
 }
 
 

@@ -205,6 +205,17 @@ SMALL = {
     "tau_one": _small(
         "tau-one", tokens_per_frame=64, n_frames=(20,), n_text=(64,),
         n_sys=(0,), tau_p=1.0),
+    # three query heads per kv head: the odd head runs as paired items
+    # (two visual blocks, or the same chunk of two query-token blocks, per
+    # work-group), each half skipping what its own rows did not retain
+    "odd_group_struct": _small(
+        "odd-group-struct", hq=6, hkv=2, n_frames=(9, 40, 5),
+        n_text=(64, 70, 130), n_sys=(5, 0, 70), n_videos=3,
+        key_struct=(2.0, 2.0, 0.8)),
+    "odd_group_fp32": _small(
+        "odd-group-fp32", dtype="fp32", d=64, hq=3, hkv=1,
+        tokens_per_frame=16, n_frames=(48,), n_text=(100,), n_sys=(3,),
+        key_struct=(2.0, 2.0, 0.8), tau_p=TAU),
 }
 
 
