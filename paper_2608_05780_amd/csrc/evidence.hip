@@ -149,36 +149,46 @@ __global__ __launch_bounds__(kCeThreads) void combine_evidence_kernel(
     // ---- evidence: frames [f0, f0 + 64) of head h
     const int h = bid / n_fb, f0 = (bid % n_fb) * kEvFrames;
     const int fl = tid % kEvFrames, rg = tid / kEvFrames;
-    const int f = f0 + fl;
+    const int f = f0 + fl, fv = min(f, pl.T - 1);
+    const int n0 = pl.frame_seq[f0];
+    const int n1 = pl.frame_seq[min(f0 + kEvFrames, pl.T) - 1];
+    const SeqDesc sq = pl.seqs[pl.frame_seq[fv]];
+    const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
+                       (fv - sq.frame0);
+    // the first rows' partial masses are in flight while the LSEs are built
+    constexpr int kPre = 8;
+    float pre[kPre];
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int r = rg + i * kEvRows;
+      pre[i] = r < sq.n_text ? src[(size_t)r * sq.n_frames] : 0.f;
+    }
     // the query rows of the videos these frames belong to are consecutive
-    const SeqDesc s0 = pl.seqs[pl.frame_seq[f0]];
-    const SeqDesc s1 = pl.seqs[pl.frame_seq[min(f0 + kEvFrames, pl.T) - 1]];
+    const SeqDesc s0 = pl.seqs[n0], s1 = pl.seqs[n1];
     const int r0 = s0.textrow0, nrows = s1.textrow0 + s1.n_text - r0;
     const bool cached = nrows <= kLseCache;
     if (cached) {
-      for (int n = pl.frame_seq[f0]; n <= pl.frame_seq[min(f0 + kEvFrames,
-                                                           pl.T) - 1]; ++n) {
-        const SeqDesc sq = pl.seqs[n];
-        for (int rr = tid; rr < sq.n_text; rr += kCeThreads)
-          l2c[sq.textrow0 - r0 + rr] = text_row_lse2(pl, ws, sq, h, rr);
+      for (int n = n0; n <= n1; ++n) {
+        const SeqDesc sn = pl.seqs[n];
+        for (int rr = tid; rr < sn.n_text; rr += kCeThreads)
+          l2c[sn.textrow0 - r0 + rr] = text_row_lse2(pl, ws, sn, h, rr);
       }
       __syncthreads();
     }
     float acc = 0.f;
     if (f < pl.T) {
-      const SeqDesc sq = pl.seqs[pl.frame_seq[f]];
-      const float* src = ws.seg + (size_t)h * pl.segtot + sq.segbase +
-                         (f - sq.frame0);
       const float* l2 = l2c + (sq.textrow0 - r0);
-      if (cached) {
-#pragma unroll 4
-        for (int r = rg; r < sq.n_text; r += kEvRows)
-          acc += exp2_(src[(size_t)r * sq.n_frames] - l2[r]);
-      } else {
-        for (int r = rg; r < sq.n_text; r += kEvRows)
-          acc += exp2_(src[(size_t)r * sq.n_frames] -
-                       text_row_lse2(pl, ws, sq, h, r));
+      auto lse = [&](int r) {
+        return cached ? l2[r] : text_row_lse2(pl, ws, sq, h, r);
+      };
+#pragma unroll
+      for (int i = 0; i < kPre; ++i) {
+        const int r = rg + i * kEvRows;
+        if (r < sq.n_text) acc += exp2_(pre[i] - lse(r));
       }
+#pragma unroll 4
+      for (int r = rg + kPre * kEvRows; r < sq.n_text; r += kEvRows)
+        acc += exp2_(src[(size_t)r * sq.n_frames] - lse(r));
     }
     red[rg][fl] = acc;
     __syncthreads();
