@@ -45,12 +45,14 @@
 //                      transpose read: within 16 lanes, lane i receives
 //                      element i % 4 of the rows addressed by lanes i/4 + 4k).
 //
-// bf16 Q and O pass through LDS in the K-tile layout: the item's Q rows are
-// read as whole 256-byte rows into the second buffer pair (free until the
-// first loop iteration refills it after a barrier), and the normalised O
-// rows are written back the same way after the last tile. Read or written
-// straight from the MFMA layout, every such instruction touches 32 rows
-// 7 KB apart, 16-32 bytes each.
+// bf16 Q and O pass through LDS in the K-tile layout: the item's Q rows go
+// by direct global -> LDS loads, as whole 256-byte rows, into the second
+// buffer pair (free until the first loop iteration refills it after a
+// barrier), in the same round trip as the first key/value tile (the item
+// record carries the descriptors both need), and the normalised O rows are
+// written back as whole rows after the last tile. Read or written straight
+// from the MFMA layout, every such instruction touches 32 rows 7 KB apart,
+// 16-32 bytes each.
 //
 // Visual and system rows finish in the kernel (O, LSE). Query-token rows are
 // split into chunks of key blocks (longest-first balance across the chip);
@@ -304,54 +306,11 @@ struct Bf16Path {
   }
   // Q and O move through LDS in the K-tile layout (rows of RC swizzled
   // 16-byte chunks), so that every global access is a whole row: 16 lanes
-  // cover one row of one head.
+  // cover one row of one head. Q arrives by the same direct global -> LDS
+  // loads as the key tiles.
   static constexpr bool kStaged = true;
   static constexpr int kPer = kTile * RC / kThreads;   // chunks per thread
 
-  // Staged Q in two halves, so that its global loads share a round trip
-  // with the first tile's: stage_q_load reads, for half hh < nh, rows
-  // [start[hh], start[hh]+len[hh]) of head hd[hh] into registers (rows past
-  // len repeat the last row), stage_q_store writes them to d0 / d1 (rows
-  // past len as zeros).
-  struct QStage {
-    bf16x8 v[2][kPer];
-  };
-  __device__ static void stage_q_load(QStage& st, const void* q,
-                                      const int (&start)[2],
-                                      const int (&len)[2],
-                                      const int (&hd)[2], int nh, int hq,
-                                      int tid) {
-    const __bf16* src = (const __bf16*)q;
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      if (hh < nh) {
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-          const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
-          const int r = min(row, len[hh] - 1);
-          st.v[hh][i] = *(const bf16x8*)(src + ((size_t)(start[hh] + r) * hq +
-                                                hd[hh]) * D + ch * 8);
-        }
-      }
-    }
-  }
-  __device__ static void stage_q_store(const QStage& st, EV_LDS char* d0,
-                                       EV_LDS char* d1, const int (&len)[2],
-                                       int nh, int tid) {
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      if (hh < nh) {
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-          const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
-          const bf16x8 z = {};
-          *(EV_LDS bf16x8*)((hh ? d1 : d0) +
-                            (row * RC + (ch ^ swz<kSwzK, RC>(row))) * 16) =
-              row < len[hh] ? st.v[hh][i] : z;
-        }
-      }
-    }
-  }
   // The B operand of row `row` from a staged Q tile (as load_q).
   __device__ static void load_q_lds(QFrag& qf, const EV_LDS char* src,
                                     int row, int g) {
@@ -460,13 +419,6 @@ struct F32Path {
     *(f32x4*)((float*)out + ((size_t)qpos * hq + h) * D + d0) = v;
   }
   static constexpr bool kStaged = false;
-  struct QStage {};
-  __device__ static void stage_q_load(QStage&, const void*, const int (&)[2],
-                                      const int (&)[2], const int (&)[2], int,
-                                      int, int) {}
-  __device__ static void stage_q_store(const QStage&, EV_LDS char*,
-                                       EV_LDS char*, const int (&)[2], int,
-                                       int) {}
   __device__ static void load_q_lds(QFrag&, const EV_LDS char*, int, int) {}
   __device__ static void o_to_lds(EV_LDS char*, const f32x16 (&)[D / 32],
                                   float, int, int) {}
@@ -588,15 +540,21 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     return d;
   };
 
-  // The item's Q rows go through the second buffer pair (K1 for the first
-  // head, V1 for the second), which the first loop iteration refills only
-  // after a barrier. Without top-p the first descriptor batch is fetched
-  // here, in the same round trip as the query block's descriptor.
+  // The item's Q rows go straight to the second buffer pair (K1 for the
+  // first half, V1 for the second) in the K-tile layout, which the first
+  // loop iteration refills only after a barrier; rows past a block's length
+  // repeat its last row (their results are never stored). The query blocks
+  // and the first key tile come with the item record, so these loads and
+  // the first tile's start one round trip after the kernel does. Without
+  // top-p the first descriptor batch is fetched in the same round trip.
   if constexpr (!TOPP) load_batch(0);
-  typename P::QStage qst;
-  if constexpr (P::kStaged)
-    P::stage_q_load(qst, ac.q, {qb0.start, qb1.start}, {qb0.len, qb1.len},
-                    {it.head, hd1}, nhalf, pl.hq, tid);
+  if constexpr (P::kStaged) {
+    TileLoader<T, D, kSwzK> qload;
+    qload.init(pl.hq, wave, lane);
+    qload.issue(kbuf(1), (const T*)ac.q, it.q0start, it.q0len, it.head, wave);
+    if (nhalf > 1)
+      qload.issue(vbuf(1), (const T*)ac.q, it.q1start, it.q1len, hd1, wave);
+  }
 
   // Top-p: a candidate tile is kept when it is always visible (system
   // prefix, the query block itself) or some row of the item's heads
@@ -684,14 +642,17 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     mx = pair_max(mx);
     const float m_new = fmaxf(m_ref, mx * c2);
     const bool need = m_new > m_ref + kRescaleSlack;
-    if (__any(need)) {
-      const float alpha = need ? exp2_(m_ref - m_new) : 1.f;
+    // While m_ref is -inf nothing has been accumulated yet (the item's
+    // first tile with a finite score): then only the reference moves.
+    const bool resc = need && m_ref != neg_inf();
+    if (__any(resc)) {
+      const float alpha = resc ? exp2_(m_ref - m_new) : 1.f;
       l_part *= alpha;
       nv_part *= alpha;
 #pragma unroll
       for (int i = 0; i < D / 32; ++i) o[i] *= alpha;
-      m_ref = need ? m_new : m_ref;
     }
+    m_ref = need ? m_new : m_ref;
   };
   auto tile_main = [&](f32x16 (&s)[2]) -> float {
     const float mu = m_ref == neg_inf() ? 0.f : m_ref;
@@ -776,17 +737,24 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
 
   // Tile j+1 streams into the other buffer pair while tile j is computed.
   if constexpr (TOPP) load_batch(0);
-  BlockDesc kb = desc(0);
-  int lnext = loc_of(0), pnext = pos_of(0);
-  unsigned wnext = 0u;
+  BlockDesc kb;
+  if constexpr (TOPP) {
+    kb = desc(0);
+  } else {
+    kb.start = it.k0start;
+    kb.len = it.k0len;
+  }
   if (n > 0) {
     kload.issue(kbuf(0), kg, kb.start, kb.len, kvh, wave);
     vload.issue(vbuf(0), vg, kb.start, kb.len, kvh, wave);
-    if (TOPP) wnext = row_bits(lnext);
   }
+  if constexpr (!TOPP) kb = desc(0);
+  int lnext = loc_of(0), pnext = pos_of(0);
+  unsigned wnext = 0u;
+  if (TOPP && n > 0) wnext = row_bits(lnext);
   if constexpr (P::kStaged) {
-    P::stage_q_store(qst, kbuf(1), vbuf(1), {qb0.len, qb1.len}, nhalf, tid);
-    __syncthreads();   // staged Q visible to every wave
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();   // Q rows visible to every wave
     P::load_q_lds(qf, hsub ? vbuf(1) : kbuf(1), qrow, g);
   }
   // Tile j lives in buffer pair j % 2. The loop is unrolled by two so that

@@ -376,6 +376,23 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     }
   // drop trailing padding
   while (!P.items.empty() && P.items.back().qblock < 0) P.items.pop_back();
+  for (WorkItem& w : P.items) {
+    if (w.qblock < 0) continue;
+    const BlockDesc& a = P.blocks[w.qblock];
+    const BlockDesc& b = P.blocks[w.qblock2 >= 0 ? w.qblock2 : w.qblock];
+    w.q0start = a.start;
+    w.q0len = a.len;
+    w.q1start = b.start;
+    w.q1len = b.len;
+    w.k0start = 0;
+    w.k0len = 1;
+    if (w.kb_end > w.kb_begin) {
+      const BlockDesc& k = w.qblock2 >= 0 ? P.ptile_desc[w.kb_begin]
+                                          : P.col_desc[w.kb_begin];
+      w.k0start = k.start;
+      w.k0len = k.len;
+    }
+  }
   for (const WorkItem& w : P.items)
     P.max_item_candidates =
         std::max(P.max_item_candidates, w.kb_end - w.kb_begin);

@@ -57,6 +57,12 @@ struct WorkItem {
   int32_t nch;       // chunks of this query-token row (0 for other rows)
   int32_t qblock2;   // -1, or the second query block of a paired item
   int32_t slot2;     // paired query-token item: qblock2's slot, else -1
+  // Copies of the descriptors the kernel needs before its first loads, so
+  // that the query rows and the first key/value tile are fetched right
+  // after the item itself: the two halves' query blocks (start token,
+  // length) and the item's first key tile (static rule).
+  int32_t q0start, q0len, q1start, q1len;
+  int32_t k0start, k0len;
 };
 
 // Key tile of a paired item: the key block and its CSR position in the row
