@@ -29,10 +29,17 @@
 //   mask               only on tiles reaching past the first query row or
 //                      shorter than 64 keys: keys after the row (causal) and
 //                      past the block end.
-//   online softmax     base-2 with log2(e) folded into the scale; the running
-//                      reference max is only moved when the tile max exceeds
-//                      it by more than 2^8, which keeps every probability
-//                      below 256 and skips almost all accumulator rescales.
+//   online softmax     base-2 with log2(e) folded into the scale. A row's
+//                      running reference m_ref is set from the exact row max
+//                      of its first tile; later tiles take their
+//                      probabilities against m_ref directly, with no row max,
+//                      and only when one of them exceeds 2^64 (or is not
+//                      finite) is the tile recomputed from the staged K tile,
+//                      its row max taken and m_ref moved (accumulators
+//                      rescaled). The reference is never above the true
+//                      running max, so the row sum stays >= 1; fp32
+//                      accumulators and bf16 P keep their relative precision
+//                      at any such scale.
 //   evidence           query-token rows only: the fp32 probabilities of each
 //                      anchor frame's keys (frames of N_v | 64 keys never cross
 //                      a tile) are summed and written once per (row, frame) as
@@ -81,6 +88,11 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
+// Probabilities taken against a stale reference may reach 2^kFastSlack
+// before the reference is moved (fp32 accumulators and the bf16 P keep
+// their relative precision at any such scale).
+constexpr float kFastSlack = 64.0f;
+constexpr float kFastBound = 18446744073709551616.0f;   // 2^kFastSlack
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_inff(); }
 __device__ __forceinline__ float exp2_(float x) {
@@ -613,8 +625,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   //         the (rare) lazy rescale of the accumulators;
   //   main: p = exp2(s * scale - m_ref) in place, row-sum partial;
   //   post: evidence partials of query-token rows, then O^T += V^T P^T.
-  auto tile_pre = [&](f32x16 (&s)[2], const BlockDesc& cur, unsigned rbit,
-                      int rloc) {
+  auto tile_mask = [&](f32x16 (&s)[2], const BlockDesc& cur, unsigned rbit,
+                       int rloc) {
     if (TOPP && rloc >= 0) {   // history block: rows that did not retain it
       const bool kept = (rbit >> (rloc & 31)) & 1u;
       if (__any(!kept)) {
@@ -634,6 +646,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         for (int r = 0; r < 16; ++r)
           if (32 * c + 8 * (r >> 2) + (r & 3) > x) s[c][r] = neg_inf();
     }
+  };
+  auto tile_ref = [&](const f32x16 (&s)[2]) {
     float mx = neg_inf();
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -665,7 +679,6 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         s[c][r] = p;
         ts += p;
       }
-    l_part += ts;
     return ts;
   };
   // query-token rows: this video's offsets (read once, outside the loop)
@@ -785,8 +798,28 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     if (active && pcur >= 0) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
       P::qk(s, kc, qf, l32, g);
-      tile_pre(s, cur, wcur, lcur);
-      const float ts = tile_main(s);
+      tile_mask(s, cur, wcur, lcur);
+      // Once every row of the wave has a reference, the tile's
+      // probabilities are taken against it without the tile's row max; the
+      // max is needed only if some probability exceeds 2^kFastSlack (or is
+      // not finite), and then the tile is recomputed from the staged K tile.
+      bool exact = __any(m_ref == neg_inf());
+      float ts = 0.f;
+      if (!exact) {
+        ts = tile_main(s);
+        exact = __any(!(ts <= kFastBound));
+        if (exact) {
+          s[0] = f32x16{};
+          s[1] = f32x16{};
+          P::qk(s, kc, qf, l32, g);
+          tile_mask(s, cur, wcur, lcur);
+        }
+      }
+      if (exact) {
+        tile_ref(s);
+        ts = tile_main(s);
+      }
+      l_part += ts;
       tile_post(s, cur, ts, vc, pcur);
     }
   };
