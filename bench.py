@@ -15,7 +15,7 @@ aggregation and top-16 frames). Inputs are resident in HBM before timing.
 Prints one JSON line: probe tokens/s (value), ms per step, the attention
 kernel's roofline against the bf16 MFMA peak (active-block FLOPs over the
 kernel's HIP-event time, measured over the timed region, where only that
-kernel is bracketed by events, on every 9th prefill call), the other
+kernel is bracketed by events, on every 27th prefill call), the other
 kernels' times from two further untimed steps, and the fp64 CPU oracle's
 throughput on a bounded sample (whole layers, at least 10 s) as a
 baseline.
@@ -304,7 +304,7 @@ def main():
     # launch would lengthen the step by about 5 %. The per-kernel breakdown
     # comes from two further, untimed steps.
     calls = args.steps * L
-    stride = max(1, min(9, calls // 4))
+    stride = max(1, min(27, calls // 4))
     ev.profile_begin(-(-calls // stride), all_kernels=False, stride=stride)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
