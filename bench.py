@@ -153,6 +153,99 @@ def cue_record(w, st, S, T, prof):
             "achieved_GBps": (intra_bytes + pair_bytes) / (ms * 1e-3) / 1e9}
 
 
+def coarse_work(ev, mask, w):
+    """Algorithmic work of one layer of coarse evidence: the block
+    affinities of every row against its history (MFMA on the mean keys'
+    bf16 hi and lo parts), the exact logits of its own block's causal prefix
+    and the video's system prefix (MFMA), and the bytes it must move at least
+    (Q read by the retention and by the coarse pass, K read by the mean-key
+    pooling, the evidence row written)."""
+    import numpy as np
+    ex = ev.mask_export(mask)
+    flop = 0.0
+    parts = 2 if w.dtype == "bf16" else 1
+    for n in np.unique(ex["video"]):
+        ids = np.nonzero(ex["video"] == n)[0]
+        sys_len = int(ex["len"][ids][ex["region"][ids] == 0].sum())
+        sel = ids[ex["region"][ids] != 0]
+        for i, b in enumerate(sel):
+            rows = int(ex["len"][b])
+            # history: the selectable blocks before b; exact part: the
+            # system prefix and the causal prefix of b (rows x (rows+1)/2)
+            flop += 2.0 * w.d * w.hq * (parts * rows * i + rows * sys_len +
+                                        rows * (rows + 1) / 2)
+    esz = 2 if w.dtype == "bf16" else 4
+    S, T = mask.stats["n_tokens"], mask.stats["n_frames_total"]
+    nbytes = (2 * S * w.hq * w.d * esz + S * w.hkv * w.d * esz +
+              w.hq * T * 4)
+    return flop, nbytes
+
+
+def coarse_main(args, ev, w, mask, qs, kks, evid, e_qf, kk, topk, ws,
+                stream, S, T, L, ks, core):
+    """--coarse: the paper's coarse query-frame evidence of every layer
+    (the retention kernels plus the coarse pass), then the frame
+    aggregation and top-k; timed like the exact probe, with HIP events
+    around every layer's coarse call on the caller's stream."""
+    import numpy as np
+    import torch
+
+    def step(evs=None):
+        for l in range(L):
+            if evs is not None:
+                evs[l][0].record(stream)
+            ev.coarse_evidence(mask, qs[l], kks[l], evid[l], ws,
+                               softmax_scale=w.softmax_scale, stream=stream)
+            if evs is not None:
+                evs[l][1].record(stream)
+        ev.frame_evidence(mask, evid, L, e_qf, k_per_seq=kk, topk=topk,
+                          stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    # per-layer times of the coarse call from one further, bracketed step
+    evs = [(torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in range(L)]
+    step(evs)
+    torch.cuda.synchronize()
+    layer_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    flop, nbytes = coarse_work(ev, mask, w)
+    found = sorted(topk[:sum(ks)].cpu().numpy().tolist())
+    rec = {
+        "metric": "coarse-evidence probe tokens/sec (top-p retention + "
+                  "coarse query-frame evidence)",
+        "value": S / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) Q/K/V, planted frames)",
+        "config": {"workload": w.name, "layers": L, "tokens": S,
+                   "frames": T, "tokens_per_frame": w.tokens_per_frame,
+                   "hq": w.hq, "hkv": w.hkv, "head_dim": w.d,
+                   "block": w.block, "tau_p": w.tau_p,
+                   "parallelism": "single-gpu"},
+        "coarse": {"ms_per_layer": layer_ms,
+                   "algorithmic_flop_per_layer": flop,
+                   "algorithmic_bytes_per_layer": nbytes,
+                   "achieved_TFLOPs": flop / (layer_ms * 1e-3) / 1e12,
+                   "achieved_GBps": nbytes / (layer_ms * 1e-3) / 1e9},
+        "topk_planted_recovered": found == sorted(core.tolist()),
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def _world():
     return int(os.environ.get("WORLD_SIZE", "1")), int(os.environ.get("RANK",
                                                                       "0"))
@@ -205,6 +298,11 @@ def main():
     ap.add_argument("--tau-p", type=float, default=0.0,
                     help="adaptive top-p retention threshold (0: the "
                          "workload's static rule)")
+    ap.add_argument("--coarse", action="store_true",
+                    help="with --tau-p: the paper's coarse query-frame "
+                         "evidence instead of the exact sparse pass (no "
+                         "attention output); one step = the coarse evidence "
+                         "of every layer plus the frame aggregation")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes "
                          "(3 times), to scale HBM byte counters")
@@ -235,6 +333,9 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 3}))
         return
     ev.load()
+    if args.coarse and (args.tau_p <= 0 or args.cues):
+        print("--coarse needs --tau-p > 0 and no --cues", file=sys.stderr)
+        sys.exit(2)
     w = wl.get(args.config, tau_p=args.tau_p) if args.tau_p > 0 else \
         wl.get(args.config)
     L = w.n_layers
@@ -294,6 +395,11 @@ def main():
                               frame_pairs=pairs, intra_frame=intra)
         ev.frame_evidence(mask, evid, L, e_qf, k_per_seq=kk, topk=topk,
                           stream=stream, frame_pairs=pairs, e_ff=e_ff)
+
+    if args.coarse:
+        coarse_main(args, ev, w, mask, qs, kks, evid, e_qf, kk, topk, ws,
+                    stream, S, T, L, ks, core)
+        return
 
     for _ in range(args.warmup):
         step()
