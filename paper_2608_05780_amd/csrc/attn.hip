@@ -625,9 +625,11 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   //         the (rare) lazy rescale of the accumulators;
   //   main: p = exp2(s * scale - m_ref) in place, row-sum partial;
   //   post: evidence partials of query-token rows, then O^T += V^T P^T.
-  auto tile_mask = [&](f32x16 (&s)[2], const BlockDesc& cur, unsigned rbit,
-                       int rloc) {
-    if (TOPP && rloc >= 0) {   // history block: rows that did not retain it
+  // Top-p: the rows of the wave that did not retain this history block
+  // (rloc >= 0) are masked whole. Only the exact path needs this; the fast
+  // path below drops such rows through their exponent offset.
+  auto row_mask = [&](f32x16 (&s)[2], unsigned rbit, int rloc) {
+    if (TOPP && rloc >= 0) {
       const bool kept = (rbit >> (rloc & 31)) & 1u;
       if (__any(!kept)) {
 #pragma unroll
@@ -636,6 +638,8 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
           for (int r = 0; r < 16; ++r) s[c][r] = kept ? s[c][r] : neg_inf();
       }
     }
+  };
+  auto tile_mask = [&](f32x16 (&s)[2], const BlockDesc& cur) {
     if (cur.len < kTile || cur.start + cur.len - 1 > qb.start) {
       // key kl = 32c + 8(r/4) + 4g + r%4 is masked when kl >= len or
       // start + kl > qpos, i.e. when its lane-free part exceeds x
@@ -668,8 +672,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     }
     m_ref = need ? m_new : m_ref;
   };
-  auto tile_main = [&](f32x16 (&s)[2]) -> float {
-    const float mu = m_ref == neg_inf() ? 0.f : m_ref;
+  auto tile_main = [&](f32x16 (&s)[2], float mu) -> float {
     float ts = 0.f;
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -798,7 +801,7 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
     if (active && pcur >= 0) {
       f32x16 s[2] = {f32x16{}, f32x16{}};
       P::qk(s, kc, qf, l32, g);
-      tile_mask(s, cur, wcur, lcur);
+      tile_mask(s, cur);
       // Once every row of the wave has a reference, the tile's
       // probabilities are taken against it without the tile's row max; the
       // max is needed only if some probability exceeds 2^kFastSlack (or is
@@ -806,18 +809,23 @@ attn_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       bool exact = __any(m_ref == neg_inf());
       float ts = 0.f;
       if (!exact) {
-        ts = tile_main(s);
+        // top-p: a row that did not retain this history block gets an
+        // offset of +inf, so all its probabilities are 0
+        const bool drop =
+            TOPP && lcur >= 0 && !((wcur >> (lcur & 31)) & 1u);
+        ts = tile_main(s, drop ? __builtin_inff() : m_ref);
         exact = __any(!(ts <= kFastBound));
         if (exact) {
           s[0] = f32x16{};
           s[1] = f32x16{};
           P::qk(s, kc, qf, l32, g);
-          tile_mask(s, cur, wcur, lcur);
+          tile_mask(s, cur);
         }
       }
       if (exact) {
+        row_mask(s, wcur, lcur);
         tile_ref(s);
-        ts = tile_main(s);
+        ts = tile_main(s, m_ref == neg_inf() ? 0.f : m_ref);
       }
       l_part += ts;
       tile_post(s, cur, ts, vc, pcur);
