@@ -442,8 +442,12 @@ __device__ __forceinline__ void affinity_tiles(
   }
 }
 
+// Four waves per SIMD (at most 128 registers): the per-row bisection is a
+// chain of dependent VALU steps and reductions, and more resident waves hide
+// its latency better than the registers an unconstrained allocation keeps.
 template <bool F32, int D, int TPR>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(
+__global__ __launch_bounds__(kSelThreads)
+__attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
     const DevPlan pl, const Workspace ws, const SelCall sc) {
   constexpr int RPW = kSelThreads / TPR;          // rows per pass
   constexpr int NRG = RPW >= 32 ? RPW / 32 : 1;   // 32-row MFMA groups
