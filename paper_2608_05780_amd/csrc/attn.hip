@@ -347,18 +347,23 @@ struct Bf16Path {
             __builtin_convertvector(v, bf16x4);
       }
   }
-  // Rows [start, start+len) of head h from a staged O tile to out.
+  // Rows [start, start+len) of head h from a staged O tile to out, as
+  // non-temporal stores: O is not read again here, and streaming it keeps
+  // the key/value tiles that other work-groups re-read in L2.
   __device__ static void o_from_lds(void* out, const EV_LDS char* src,
                                     int start, int len, int h, int hq,
                                     int tid) {
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int slot = i * kThreads + tid, row = slot / RC, ch = slot % RC;
-      if (row < len)
-        *(bf16x8*)((__bf16*)out + ((size_t)(start + row) * hq + h) * D +
-                   ch * 8) =
-            *(const EV_LDS bf16x8*)(src + (row * RC +
-                                           (ch ^ swz<kSwzK, RC>(row))) * 16);
+      if (row < len) {
+        typedef int i32x4 __attribute__((ext_vector_type(4)));
+        const i32x4 v = *(const EV_LDS i32x4*)(src + (row * RC +
+                                                (ch ^ swz<kSwzK, RC>(row))) * 16);
+        __builtin_nontemporal_store(
+            v, (i32x4*)((__bf16*)out + ((size_t)(start + row) * hq + h) * D +
+                        ch * 8));
+      }
     }
   }
 };
