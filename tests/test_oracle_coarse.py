@@ -86,6 +86,10 @@ def test_coarse_map_loops():
     tau, scale = 0.75, 0.5
     P, keep, blk = _coarse_full(q, k, lay, B, tau, scale)
     nb = int(blk.count[0])
+    # query-frame evidence of the coarse map, looped: the query rows
+    # (tokens past the system prefix and the frames) summed per frame
+    vis0, txt0 = ns[0], ns[0] + nf[0] * Nv
+    E = np.zeros((2, nf[0]))
     for h in range(2):
         for i in range(lay.S):
             lb = int(blk.local[i])
@@ -121,6 +125,15 @@ def test_coarse_map_loops():
             for m, x in logits.items():
                 want[m] = math.exp(x - mx) / z
             np.testing.assert_allclose(P[h, i], want, rtol=0, atol=1e-13)
+            if i >= txt0:
+                for m in range(vis0, txt0):
+                    E[h, (m - vis0) // Nv] += want[m]
+    # the oracle's query_frame from the groups of every row (rows that are
+    # not query tokens must contribute nothing)
+    rows = np.arange(lay.S)
+    groups = coarse.coarse_probs(q, k, lay, blk, keep, rows, scale)
+    np.testing.assert_allclose(coarse.query_frame(lay, groups, 2), E,
+                               rtol=0, atol=1e-12)
 
 
 def test_metrics_against_scipy_and_closed_forms():

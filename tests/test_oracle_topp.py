@@ -234,6 +234,17 @@ def test_attention_under_retention_bruteforce():
     tau, scale = 0.6, 0.5
     res = topp.run_layer(q, k, v, lay, B, tau, scale)
     keep = res["keep"]
+    # token roles from the layout numbers alone: (video, region, global
+    # frame) of every token, region 0 system, 1 visual, 2 query
+    role = []
+    f0 = 0
+    for n in range(len(ns)):
+        role += [(n, 0, -1)] * ns[n]
+        role += [(n, 1, f0 + t // Nv) for t in range(nf[n] * Nv)]
+        role += [(n, 2, -1)] * nt[n]
+        f0 += nf[n]
+    E = [[0.0] * f0 for _ in range(hq)]
+    tm = [[0.0] * len(ns) for _ in range(hq)]
     for h in range(hq):
         for i in range(lay.S):
             kept = set(np.nonzero(keep[h, i])[0].tolist())
@@ -252,7 +263,17 @@ def test_attention_under_retention_bruteforce():
             np.testing.assert_allclose(res["O"][i, h], o, rtol=0, atol=1e-12)
             lse = max(s) + math.log(math.fsum(math.exp(x - max(s)) for x in s))
             assert abs(res["LSE"][h, i] - lse) < 1e-12
-    # evidence: per head, frame masses plus the rest = number of query rows
+            # evidence (Evidence Decomposition, query-frame cue): a query
+            # row's mass on each frame's visual keys, the rest to text_mass
+            if role[i][1] == 2:
+                for x, m in enumerate(keys):
+                    if role[m][1] == 1:
+                        E[h][role[m][2]] += p[x]
+                    else:
+                        tm[h][role[i][0]] += p[x]
+    np.testing.assert_allclose(res["E"], E, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(res["text_mass"], tm, rtol=0, atol=1e-12)
+    # per head, frame masses plus the rest = number of query rows
     tot = res["E"].sum(axis=1) + res["text_mass"].sum(axis=1)
     np.testing.assert_allclose(tot, lay.n_text.sum(), rtol=0, atol=1e-12)
 
