@@ -72,6 +72,20 @@ def measured_traffic():
     return None
 
 
+def allowed_token_pairs(ev, mask):
+    """Token pairs (query, key) the static rule allows, per head and layer:
+    a key block before the query block is visible whole, the diagonal block
+    causally (len * (len + 1) / 2 pairs)."""
+    import numpy as np
+    ex = ev.mask_export(mask)
+    ln = ex["len"].astype(np.int64)
+    rows = np.repeat(np.arange(len(ln)), np.diff(ex["row_ptr"]))
+    col = ex["col"].astype(np.int64)
+    diag = rows == col
+    return float(np.where(diag, ln[rows] * (ln[rows] + 1) // 2,
+                          ln[rows] * ln[col]).sum())
+
+
 def work_units(ev, mask):
     """The attention work list as (query block, first head, heads, CSR run)
     units: an ordinary item is one unit; a paired item (one head over two
@@ -437,6 +451,9 @@ def main():
         flop_layer = tile_flop * w.hq * st["n_active_pairs"]
     attn_ms = prof_attn["attention_ms"] / max(1, prof_attn["calls"])
     achieved = flop_layer / (attn_ms * 1e-3) / 1e12
+    # strict count: 4 d flop per allowed (query, key) token pair and head
+    strict_flop = (4.0 * w.d * w.hq * allowed_token_pairs(ev, mask)
+                   if w.tau_p == 0 else None)
     # combine + evidence kernel: the query rows' per-frame partial masses
     # and the evidence row, the chunk partials (O, reference max, row sum,
     # non-visual mass), the merged O and LSE of the query rows
@@ -475,9 +492,18 @@ def main():
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms,
                      "timed_launches": prof_attn["calls"]},
+        "strict_allowed_pairs": (None if strict_flop is None else {
+            "flop_per_launch": strict_flop,
+            "achieved_TFLOPs": strict_flop / (attn_ms * 1e-3) / 1e12,
+            "frac": strict_flop / (attn_ms * 1e-3) / 1e12 /
+                    PEAK_BF16_TFLOPS}),
+        # kernels the step does not launch are null, not the empty span
+        # between their events
         "kernels_ms_per_layer": {
-            "cues": prof["cues_ms"] / max(1, prof["calls"]),
-            "retention": prof["select_ms"] / max(1, prof["calls"]),
+            "cues": (prof["cues_ms"] / max(1, prof["calls"])
+                     if args.cues else None),
+            "retention": (prof["select_ms"] / max(1, prof["calls"])
+                          if w.tau_p > 0 else None),
             "attention": attn_ms,
             "combine_evidence": ev_ms},
         "evidence_reduce_GBps": ev_bytes / (ev_ms * 1e-3) / 1e9,

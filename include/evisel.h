@@ -109,9 +109,14 @@ typedef struct {
 /* Builds the block partition, the compact list of active block pairs (CSR,
  * each row's key blocks in increasing order) and the attention work list
  * for Hq query heads and Hkv kv heads, then uploads them to the current
- * device with a copy on `stream` (the call waits for that copy). *out is
- * library-owned; release it with evisel_mask_free. Errors: INVALID_ARG for
- * a bad layout or rule or hq % hkv != 0, NOMEM, HIP. */
+ * device. The upload is an asynchronous copy on `stream` from a pinned
+ * host buffer the mask owns; the call does not wait for it. Compute calls
+ * on the same stream are ordered after it; a caller that uses the mask on
+ * another stream first synchronizes `stream` (or orders the other stream
+ * after it). The device allocation and the pinned buffer are made here,
+ * once per mask. *out is library-owned; release it with evisel_mask_free.
+ * Errors: INVALID_ARG for a bad layout or rule or hq % hkv != 0, NOMEM,
+ * HIP. */
 evisel_status evisel_build_block_mask(const evisel_layout* layout,
                                       const evisel_mask_rule* rule,
                                       int32_t hq, int32_t hkv, void* stream,
@@ -125,9 +130,21 @@ evisel_status evisel_build_block_mask_host(const evisel_layout* layout,
                                            int32_t hq, int32_t hkv,
                                            evisel_mask** out);
 
-/* Frees host and device memory of a mask (NULL is ignored). The caller must
- * make sure no queued work still reads it. */
+/* Frees host and device memory of a mask (NULL is ignored). It waits for
+ * the mask's own upload copy; the caller must make sure no queued kernel
+ * still reads the mask. */
 void evisel_mask_free(evisel_mask* mask);
+
+/* Reorders the attention work list: item i of the new launch order is item
+ * perm[i] of the current one (perm: host [n_work_items], a permutation).
+ * Every output of evisel_sparse_prefill has exactly one writer and every
+ * reduction runs in a fixed order, so results do not depend on the launch
+ * order; this call lets a caller check that (for example with the order
+ * reversed). It waits for the mask's previous upload, then copies the new
+ * work list asynchronously on `stream`. Errors: INVALID_ARG (host-only mask,
+ * NULL perm, not a permutation), HIP. */
+evisel_status evisel_mask_permute_work(evisel_mask* mask, const int32_t* perm,
+                                       void* stream);
 
 evisel_status evisel_mask_info(const evisel_mask* mask, evisel_mask_stats* out);
 

@@ -24,7 +24,7 @@ __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "select_blocks", "unpack_row_bits", "mask_export_pairs",
            "coarse_evidence",
            "mask_info", "mask_export", "mask_export_work",
-           "mask_export_paired", "profile_begin",
+           "mask_export_paired", "mask_permute_work", "profile_begin",
            "profile_end", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)),
@@ -69,6 +69,8 @@ _SIGS = {
         ctypes.POINTER(_Layout), ctypes.POINTER(_Rule), ctypes.c_int32,
         ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
     "evisel_mask_free": (None, [ctypes.c_void_p]),
+    "evisel_mask_permute_work": (ctypes.c_int, [ctypes.c_void_p, _i32p,
+                                                ctypes.c_void_p]),
     "evisel_mask_info": (ctypes.c_int, [ctypes.c_void_p,
                                         ctypes.POINTER(_Stats)]),
     "evisel_mask_export": (ctypes.c_int, [ctypes.c_void_p] + [_i32p] * 6),
@@ -233,6 +235,17 @@ def mask_export_work(mask: Mask) -> dict:
     _check(load().evisel_mask_export_work(mask.handle,
                                           *[p(out[k]) for k in keys]))
     return {k: v[:n] for k, v in out.items()}
+
+
+def mask_permute_work(mask: Mask, perm, stream=None):
+    """New launch order of the attention work list: item i is the current
+    item perm[i] (a permutation of range(n_work_items))."""
+    import numpy as np
+    p = np.ascontiguousarray(np.asarray(perm, np.int32))
+    if p.size != mask.stats["n_work_items"]:
+        raise ValueError("perm needs one entry per work item")
+    _check(load().evisel_mask_permute_work(mask.handle, p.ctypes.data_as(_i32p),
+                                           _stream(stream)))
 
 
 def mask_export_paired(mask: Mask) -> dict:

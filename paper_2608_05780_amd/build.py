@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libevisel.so")
-SOURCES = ["api.hip", "attn.hip", "evidence.hip", "select.hip", "plan.cpp"]
+SOURCES = ["api.hip", "attn.hip", "attn_pipe.hip", "evidence.hip", "select.hip",
+           "plan.cpp"]
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # no packed-fp32 VALU instructions anywhere in device code

@@ -11,7 +11,11 @@
 
 struct evisel_mask {
   evisel::Plan plan;
-  void* dev = nullptr;  // one device allocation holding every table
+  void* dev = nullptr;      // one device allocation holding every table
+  void* staging = nullptr;  // pinned host copy the upload reads from
+  size_t bytes = 0;         // size of both
+  size_t items_off = 0;     // offset of the work-item table in both
+  hipEvent_t uploaded = nullptr;  // recorded after the last upload copy
   evisel::DevPlan dp{};
   int device = -1;
 };
@@ -109,8 +113,26 @@ evisel_status upload(evisel_mask* m, hipStream_t s) {
     return e == hipErrorOutOfMemory ? fail(EVISEL_ERR_NOMEM, "hipMalloc")
                                     : hip_fail(e, "hipMalloc");
   }
-  e = hipMemcpyAsync(m->dev, buf.data(), buf.size(), hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  // The copy reads a pinned staging buffer that the mask keeps until it is
+  // freed, so the call returns without waiting for it; the event marks its
+  // completion for evisel_mask_free and evisel_mask_permute_work.
+  e = hipHostMalloc(&m->staging, buf.size(), hipHostMallocDefault);
+  if (e != hipSuccess) {
+    m->staging = nullptr;
+    return e == hipErrorOutOfMemory ? fail(EVISEL_ERR_NOMEM, "hipHostMalloc")
+                                    : hip_fail(e, "hipHostMalloc");
+  }
+  std::memcpy(m->staging, buf.data(), buf.size());
+  m->bytes = buf.size();
+  m->items_off = o_it;
+  e = hipEventCreateWithFlags(&m->uploaded, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    m->uploaded = nullptr;
+    return hip_fail(e, "hipEventCreate");
+  }
+  e = hipMemcpyAsync(m->dev, m->staging, buf.size(), hipMemcpyHostToDevice,
+                     s);
+  if (e == hipSuccess) e = hipEventRecord(m->uploaded, s);
   if (e != hipSuccess) return hip_fail(e, "plan upload");
   char* d = (char*)m->dev;
   evisel::DevPlan& dp = m->dp;
@@ -315,8 +337,43 @@ evisel_status evisel_build_block_mask_host(const evisel_layout* layout,
 
 void evisel_mask_free(evisel_mask* mask) {
   if (!mask) return;
+  if (mask->uploaded) {
+    (void)hipEventSynchronize(mask->uploaded);   // the copy reads staging
+    (void)hipEventDestroy(mask->uploaded);
+  }
+  if (mask->staging) (void)hipHostFree(mask->staging);
   if (mask->dev) (void)hipFree(mask->dev);
   delete mask;
+}
+
+evisel_status evisel_mask_permute_work(evisel_mask* m, const int32_t* perm,
+                                       void* stream) {
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  if (!perm) return fail(EVISEL_ERR_INVALID_ARG, "null perm");
+  std::vector<evisel::WorkItem>& it = m->plan.items;
+  const size_t n = it.size();
+  std::vector<char> seen(n, 0);
+  for (size_t i = 0; i < n; ++i) {
+    if (perm[i] < 0 || (size_t)perm[i] >= n || seen[perm[i]])
+      return fail(EVISEL_ERR_INVALID_ARG,
+                  "perm is not a permutation of the work items");
+    seen[perm[i]] = 1;
+  }
+  std::vector<evisel::WorkItem> next(n);
+  for (size_t i = 0; i < n; ++i) next[i] = it[perm[i]];
+  // the previous upload may still read the staging buffer
+  hipError_t e = hipEventSynchronize(m->uploaded);
+  if (e != hipSuccess) return hip_fail(e, "plan upload wait");
+  it.swap(next);
+  char* st_items = (char*)m->staging + m->items_off;
+  if (n) std::memcpy(st_items, it.data(), n * sizeof(evisel::WorkItem));
+  hipStream_t s = (hipStream_t)stream;
+  e = hipMemcpyAsync((char*)m->dev + m->items_off, st_items,
+                     n * sizeof(evisel::WorkItem), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipEventRecord(m->uploaded, s);
+  if (e != hipSuccess) return hip_fail(e, "work list upload");
+  return EVISEL_OK;
 }
 
 evisel_status evisel_mask_info(const evisel_mask* m, evisel_mask_stats* out) {

@@ -80,6 +80,12 @@ struct AttnCall {
 
 hipError_t launch_attention(const DevPlan& p, const Workspace& w,
                             const AttnCall& c, hipStream_t s);
+// The software-pipelined attention kernel (attn_pipe.hip): bf16, d = 64 or
+// 128, static rule, no frame-cue outputs; launch_attention uses it for
+// every call it supports.
+bool attention_pipe_supported(const DevPlan& p, const AttnCall& c);
+hipError_t launch_attention_pipe(const DevPlan& p, const Workspace& w,
+                                 const AttnCall& c, hipStream_t s);
 // Top-p retention: mean keys, then per (block, head) the retained history
 // of every row (rbits) and the union over the block's rows (ubits).
 // LDS bytes the retention kernel needs at its narrowest setting.

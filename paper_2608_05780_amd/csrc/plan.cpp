@@ -386,11 +386,17 @@ std::string build_plan(const Layout& L, const Rule& R, int32_t hq, int32_t hkv,
     w.q1len = b.len;
     w.k0start = 0;
     w.k0len = 1;
+    w.k1start = 0;
+    w.k1len = 0;
+    const std::vector<BlockDesc>& kd =
+        w.qblock2 >= 0 ? P.ptile_desc : P.col_desc;
     if (w.kb_end > w.kb_begin) {
-      const BlockDesc& k = w.qblock2 >= 0 ? P.ptile_desc[w.kb_begin]
-                                          : P.col_desc[w.kb_begin];
-      w.k0start = k.start;
-      w.k0len = k.len;
+      w.k0start = kd[w.kb_begin].start;
+      w.k0len = kd[w.kb_begin].len;
+    }
+    if (w.kb_end > w.kb_begin + 1) {
+      w.k1start = kd[w.kb_begin + 1].start;
+      w.k1len = kd[w.kb_begin + 1].len;
     }
   }
   for (const WorkItem& w : P.items)

@@ -58,11 +58,13 @@ struct WorkItem {
   int32_t qblock2;   // -1, or the second query block of a paired item
   int32_t slot2;     // paired query-token item: qblock2's slot, else -1
   // Copies of the descriptors the kernel needs before its first loads, so
-  // that the query rows and the first key/value tile are fetched right
+  // that the query rows and the first key/value tiles are fetched right
   // after the item itself: the two halves' query blocks (start token,
-  // length) and the item's first key tile (static rule).
+  // length) and the item's first two key tiles (static rule; k1len = 0
+  // when the item has one tile).
   int32_t q0start, q0len, q1start, q1len;
   int32_t k0start, k0len;
+  int32_t k1start, k1len;
 };
 
 // Key tile of a paired item: the key block and its CSR position in the row

@@ -40,17 +40,22 @@ def to_device(layer: wl.Layer, w: wl.Workload, torch):
 
 
 def run_gpu(ev, w: wl.Workload, layers, seed=0, k_per_video=None,
-            keep_o=True, layer_inputs=None, on_layer=None, cues=False):
+            keep_o=True, layer_inputs=None, on_layer=None, cues=False,
+            work_order=None):
     """Run ``layers`` (list of layer ids) of workload ``w`` on the GPU.
 
     ``on_layer(j, layer_id, out, lse)`` (torch tensors on the GPU) is called
-    after each layer; with ``keep_o`` the outputs are also copied to host."""
+    after each layer; with ``keep_o`` the outputs are also copied to host.
+    ``work_order(n_items)`` returns a permutation of the attention work list
+    to launch it in (default: the plan's order)."""
     import torch
     ns, nf, nt = wl.layout_arrays(w, seed)
     mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
                                w.sink_blocks, w.window, w.hq, w.hkv,
                                n_sys=ns, tau_p=w.tau_p)
     st = mask.stats
+    if work_order is not None:
+        ev.mask_permute_work(mask, work_order(st["n_work_items"]))
     S, T, nseq = st["n_tokens"], st["n_frames_total"], len(nf)
     L = len(layers)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32

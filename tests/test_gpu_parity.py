@@ -245,6 +245,27 @@ def test_deterministic_bitwise():
     assert np.array_equal(a.text_mass, b.text_mass)
 
 
+@pytest.mark.parametrize("name", ["config2", "multi_video_d64",
+                                  "ragged_sys_bf16", "tiny_fp32"])
+def test_deterministic_reversed_work_order(name):
+    """Every output has one writer and every reduction a fixed order, so
+    launching the work list reversed gives bitwise the same results."""
+    w = wl.get(2) if name == "config2" else SMALL[name]
+    lay, _ = _lay_rule(w)
+    ks = [min(2, F) for F in lay.n_frames]
+    say(f"case reversed work order {name}")
+    a = run_gpu(pytest.ev, w, [0], k_per_video=ks)
+    b = run_gpu(pytest.ev, w, [0], k_per_video=ks,
+                work_order=lambda n: np.arange(n)[::-1])
+    assert np.array_equal(a.O[0], b.O[0])
+    assert np.array_equal(a.LSE[0], b.LSE[0])
+    assert np.array_equal(a.E, b.E)
+    assert np.array_equal(a.text_mass, b.text_mass)
+    assert np.array_equal(a.e_qf, b.e_qf)
+    for x, y in zip(a.topk, b.topk):
+        assert np.array_equal(x, y)
+
+
 def test_profile_sessions():
     """Kernel timing: with all_kernels the five spans are recorded; without,
     only the attention kernel's, and the others read 0. With a stride, only
