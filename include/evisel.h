@@ -290,6 +290,31 @@ evisel_status evisel_sparse_prefill(const evisel_mask* mask, int32_t layer,
                                     float* intra_frame, void* workspace,
                                     size_t workspace_bytes, void* stream);
 
+/* Bytes of the static workspace of evisel_sparse_prefill_noalloc, per GPU. */
+#define EVISEL_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * evisel_sparse_prefill with the same arguments and results, minus
+ * workspace and workspace_bytes. The workspace is a device array inside the
+ * library, EVISEL_NOALLOC_WORKSPACE_BYTES on every GPU the library is loaded
+ * on, held until the process ends. The call allocates nothing and clears
+ * nothing: no kernel of a call reads workspace bytes that the same call has
+ * not written, so the array keeping the previous call's contents does not
+ * matter. Every call on one GPU shares that GPU's array: calls that overlap
+ * on one GPU (two streams, or two host threads) race, and the caller must
+ * order them (e.g. one stream). The array's device address is looked up on
+ * the first call on each GPU.
+ * Errors: those of evisel_sparse_prefill; WORKSPACE when the mask (with the
+ * frame-cue workspace, when frame_pairs or intra_frame is given) needs more
+ * than EVISEL_NOALLOC_WORKSPACE_BYTES; UNSUPPORTED for a device ordinal
+ * above 63. */
+evisel_status evisel_sparse_prefill_noalloc(
+    const evisel_mask* mask, int32_t layer, int32_t n_layers, const void* q,
+    const void* k, const void* v, int32_t d, evisel_dtype dtype,
+    float softmax_scale, void* out, float* lse, float* evidence,
+    float* text_mass, float* frame_pairs, float* intra_frame, void* stream);
+
 /* Aggregates evidence [n_layers, Hq, T] (Evidence Decomposition: mean over
  * heads per layer, then the timestamp-aligned query-frame score):
  *   e_qf_layer device [n_layers, T] or NULL:

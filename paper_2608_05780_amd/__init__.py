@@ -25,6 +25,7 @@ __all__ = ["load", "EviselError", "Mask", "build_block_mask",
            "coarse_evidence",
            "mask_info", "mask_export", "mask_export_work",
            "mask_export_paired", "mask_permute_work", "profile_begin",
+           "sparse_prefill_noalloc", "NOALLOC_WORKSPACE_BYTES",
            "profile_end", "LIB_PATH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)),
@@ -84,6 +85,11 @@ _SIGS = {
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_size_t, ctypes.c_void_p]),
+    "evisel_sparse_prefill_noalloc": (ctypes.c_int, [
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "evisel_cue_workspace": (ctypes.c_size_t, [ctypes.c_void_p,
                                                ctypes.c_int32]),
     "evisel_mask_export_pairs": (ctypes.c_int, [ctypes.c_void_p, _i32p,
@@ -307,6 +313,25 @@ def sparse_prefill(mask: Mask, layer: int, n_layers: int, q, k, v, out,
         _dtype_code(q), scale, _ptr(out), _ptr(lse), _ptr(evidence),
         _ptr(text_mass), _ptr(frame_pairs), _ptr(intra_frame), _ptr(workspace),
         0 if workspace is None else workspace.numel() * workspace.element_size(),
+        _stream(stream)))
+
+
+# bytes of the library's static workspace per GPU (EVISEL_NOALLOC_WORKSPACE_BYTES)
+NOALLOC_WORKSPACE_BYTES = 64 << 20
+
+
+def sparse_prefill_noalloc(mask: Mask, layer: int, n_layers: int, q, k, v,
+                           out, evidence, lse=None, text_mass=None,
+                           softmax_scale: Optional[float] = None, stream=None,
+                           frame_pairs=None, intra_frame=None):
+    """sparse_prefill with the library's static per-GPU workspace instead of
+    a caller's (allocates nothing; calls that overlap on one GPU race)."""
+    d = int(q.shape[-1])
+    scale = float(softmax_scale) if softmax_scale is not None else d ** -0.5
+    _check(load().evisel_sparse_prefill_noalloc(
+        mask.handle, layer, n_layers, _ptr(q), _ptr(k), _ptr(v), d,
+        _dtype_code(q), scale, _ptr(out), _ptr(lse), _ptr(evidence),
+        _ptr(text_mass), _ptr(frame_pairs), _ptr(intra_frame),
         _stream(stream)))
 
 

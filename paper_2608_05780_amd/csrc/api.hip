@@ -2,6 +2,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -19,6 +20,13 @@ struct evisel_mask {
   evisel::DevPlan dp{};
   int device = -1;
 };
+
+// Workspace of evisel_sparse_prefill_noalloc. Each GPU the library is
+// loaded on holds its own copy, at its own address, until the process ends.
+// Host code uses this name only to look that address up (scratch_address);
+// the name itself is a host-side stand-in, not a device pointer.
+static __device__ __align__(256) unsigned char
+    scratch[EVISEL_NOALLOC_WORKSPACE_BYTES];
 
 namespace {
 
@@ -290,6 +298,29 @@ void prof_record(size_t call, int k, hipStream_t s) {
   (void)hipEventRecord(g_prof.ev[kProfEvents * call + k], s);
 }
 
+// Device address of `scratch` per GPU, looked up once per device, with that
+// device current, on the first no-allocation call there.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+evisel_status scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(EVISEL_ERR_UNSUPPORTED,
+                "no static workspace for device ordinals above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || ((uintptr_t)p & 255))
+      return fail(EVISEL_ERR_HIP, "static workspace is not 256-byte aligned");
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return EVISEL_OK;
+}
+
 evisel_status check_device(const evisel_mask* m) {
   if (!m) return fail(EVISEL_ERR_INVALID_ARG, "null mask");
   if (!m->dev)
@@ -544,6 +575,36 @@ evisel_status evisel_sparse_prefill(const evisel_mask* m, int32_t layer,
     g_prof.used++;
   }
   return EVISEL_OK;
+}
+
+evisel_status evisel_sparse_prefill_noalloc(
+    const evisel_mask* m, int32_t layer, int32_t n_layers, const void* q,
+    const void* k, const void* v, int32_t d, evisel_dtype dtype,
+    float softmax_scale, void* out, float* lse, float* evidence,
+    float* text_mass, float* frame_pairs, float* intra_frame, void* stream) {
+  // the mask's device is the current one (checked), so the lookup below
+  // runs with the right device current
+  evisel_status st = check_device(m);
+  if (st != EVISEL_OK) return st;
+  if (d == 64 || d == 128) {
+    const WsLayout wl = ws_layout(m->plan, d);
+    const size_t need =
+        wl.total + (frame_pairs || intra_frame ? wl.cue_total : 0);
+    if (need > EVISEL_NOALLOC_WORKSPACE_BYTES)
+      return fail(EVISEL_ERR_WORKSPACE,
+                  "this mask needs " + std::to_string(need) +
+                      " bytes of workspace; the static workspace holds " +
+                      std::to_string(EVISEL_NOALLOC_WORKSPACE_BYTES));
+  }
+  void* ws = nullptr;
+  st = scratch_address(m->device, &ws);
+  if (st != EVISEL_OK) return st;
+  // the ordinary entry point with that workspace: it allocates nothing and
+  // no kernel reads workspace bytes the same call has not written
+  return evisel_sparse_prefill(m, layer, n_layers, q, k, v, d, dtype,
+                               softmax_scale, out, lse, evidence, text_mass,
+                               frame_pairs, intra_frame, ws,
+                               EVISEL_NOALLOC_WORKSPACE_BYTES, stream);
 }
 
 size_t evisel_cue_workspace(const evisel_mask* m, int32_t d) {
