@@ -137,3 +137,30 @@ def output_error(O_gpu, O_ref, rows):
     """max |O_gpu - O_ref| / max |O_ref| over ``rows``."""
     g = O_gpu[rows].astype(np.float64)
     return float(np.abs(g - O_ref).max() / max(np.abs(O_ref).max(), 1e-30))
+
+
+def oracle_query_rows(w: wl.Workload, seed: int, qt, k, v):
+    """The oracle's evidence, non-visual mass, O and LSE of one layer's query
+    rows. ``qt`` holds q of those rows only (the oracle reads q at the rows
+    it computes and nowhere else); k and v are whole. Inputs are bf16 bit
+    patterns or fp32, as ``wl.gen_layer`` returns them. Runs in a worker
+    process: it imports neither torch nor the HIP library."""
+    from oracle.attention import evidence
+    from oracle.layout import Layout, Rule
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    lay = Layout(ns, nf, nt, w.tokens_per_frame)
+    rule = Rule(w.block, w.sink_blocks, w.window)
+    if qt.dtype == np.uint16:
+        cv = lambda a: wl.bf16_bits_to_f32(a).astype(np.float64)
+    else:
+        cv = lambda a: a.astype(np.float64)
+    q = np.zeros((lay.S,) + qt.shape[1:])
+    q[lay.text_rows()] = cv(qt)
+    E, tm, O, LSE, _ = evidence(q, cv(k), cv(v), lay, rule, w.softmax_scale)
+    return E, tm, O, LSE
+
+
+def _limit_threads(n):
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(n)
+

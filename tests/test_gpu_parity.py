@@ -19,6 +19,11 @@ from gpu_harness import run_gpu, sample_rows, output_error, say
 pytestmark = pytest.mark.gpu
 
 O_TOL, E_TOL, LSE_TOL = 2e-2, 1e-3, 2e-3
+# Full rankings of a 1024-frame video have adjacent pooled-score gaps near
+# 1e-5, below what E_TOL can decide; the all-layer tests also hold the
+# evidence to this bound (fp32 sums of fp32 probabilities; the GPU stays
+# near 1e-7) and decide ranking boundaries with it.
+E_RANK_TOL = 1e-5
 
 
 def _lay_rule(w, seed=0):
@@ -48,6 +53,40 @@ def _check_mass_invariant(res, lay):
         tot = res.E[:, :, f0:f0 + F].sum(axis=2) + res.text_mass[:, :, n]
         assert np.abs(tot - lay.n_text[n]).max() <= 1e-3 * max(
             1, lay.n_text[n] / 64)
+
+
+def _check_ranking(res, E_ref_all, lay, planted, e_tol=E_TOL):
+    """Full per-video rankings (top-k with k = the video's frame count):
+    the GPU's pooled scores against the oracle's, and, for every k at which
+    the oracle's score gap between ranks k and k+1 exceeds four times the
+    evidence tolerance ``e_tol`` propagated to the pooled score, the GPU's
+    top-k set equal to the oracle's. At least the planted count's worth of leading ranks must be
+    decided somewhere, so that the check has teeth."""
+    e_qf_ref, pooled = oracle.frame_evidence(E_ref_all, lay.n_frames,
+                                             lay.n_text)
+    tol_layer = e_tol / np.repeat(lay.n_text, lay.n_frames)
+    assert np.all(np.abs(res.e_qf_layer - e_qf_ref) <= tol_layer + 1e-9)
+    assert np.all(np.abs(res.e_qf - pooled) <= tol_layer + 1e-9)
+    F_all = [int(F) for F in lay.n_frames]
+    ref_rank = oracle.topk_per_video(pooled, lay.n_frames, F_all)
+    same_prec = oracle.topk_per_video(res.e_qf.astype(np.float32),
+                                      lay.n_frames, F_all)
+    for n in range(lay.n_seq):
+        F, f0 = F_all[n], int(lay.frame0[n])
+        g = res.topk[n]
+        np.testing.assert_array_equal(g, same_prec[n])
+        s = np.sort(pooled[f0:f0 + F])[::-1]
+        gap = s[:-1] - s[1:]                       # gap after rank k, k = 1..F-1
+        decided = np.nonzero(gap > 4 * e_tol / lay.n_text[n])[0] + 1
+        pos = np.empty(F, np.int64)
+        pos[ref_rank[n]] = np.arange(F)
+        ok = np.maximum.accumulate(pos[g]) == np.arange(F)   # prefix sets equal
+        bad = [int(k) for k in decided if not ok[k - 1]]
+        say(f"  video {n}: {F} frames, {decided.size} decided top-k "
+            f"boundaries (largest decided k <= planted {planted[n]}: "
+            f"{int(decided[decided <= planted[n]].max(initial=0))})")
+        assert not bad, (n, bad[:10])
+        assert decided.size > 0 and decided.min() <= max(1, planted[n])
 
 
 def _check_topk(res, E_ref_all, lay, ks):
@@ -232,6 +271,82 @@ def test_parity_ragged_batch_two_layers():
     """8 packed videos of 64-512 frames x 32 tokens: layers 0 and 13."""
     say("case config-5 (layers 0, 13)")
     _sampled_case(wl.get(5), [0, 13], n_rows=1024)
+
+
+def _all_layers_query_rows(w, seed=0, workers=3):
+    """Every layer of ``w``: the GPU's evidence, non-visual mass, and the O
+    and LSE of all query rows against the oracle; then the pooled scores
+    and the full per-video rankings (``_check_ranking``). The oracle runs
+    in worker processes (spawned: no GPU state), fed the layer the GPU
+    ran."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    import torch
+    from gpu_harness import oracle_query_rows, _limit_threads
+    lay, _ = _lay_rule(w, seed)
+    _, core, _ = wl.plant_table(w, seed)
+    planted = [int(((core >= f0) & (core < f0 + F)).sum())
+               for f0, F in zip(lay.frame0, lay.n_frames)]
+    ks = [int(F) for F in lay.n_frames]
+    txt = lay.text_rows()
+    tt = torch.from_numpy(txt).cuda()
+    cache, futs, gpu_rows = {}, {}, {}
+    ex = cf.ProcessPoolExecutor(workers, mp_context=mp.get_context("spawn"),
+                                initializer=_limit_threads,
+                                initargs=(max(1, 16 // workers),))
+
+    def layer_inputs(l):
+        cache.clear()
+        cache[l] = wl.gen_layer(w, l, seed)
+        return cache[l]
+
+    def on_layer(j, l, out, lse):
+        lay_l = cache[l]
+        futs[j] = ex.submit(oracle_query_rows, w, seed, lay_l.q[txt],
+                            lay_l.k, lay_l.v)
+        gpu_rows[j] = (out.index_select(0, tt).float().cpu().numpy(),
+                       lse.index_select(1, tt).cpu().numpy())
+
+    try:
+        layers = list(range(w.n_layers))
+        res = run_gpu(pytest.ev, w, layers, seed, k_per_video=ks,
+                      keep_o=False, layer_inputs=layer_inputs,
+                      on_layer=on_layer)
+        E_all, TM_all = [], []
+        for j in layers:
+            E, tm, O, LSE = futs[j].result()
+            o_g, lse_g = gpu_rows[j]
+            err = float(np.abs(o_g - O).max() / np.abs(O).max())
+            lse_err = float(np.abs(lse_g - LSE).max())
+            e_err = float(np.abs(res.E[j] - E).max())
+            t_err = float(np.abs(res.text_mass[j] - tm).max())
+            say(f"  layer {j}: query rows O {err:.2e}  LSE {lse_err:.2e}  "
+                f"E {e_err:.2e}  text_mass {t_err:.2e}")
+            assert err <= O_TOL and lse_err <= LSE_TOL
+            assert e_err <= E_RANK_TOL and t_err <= E_RANK_TOL
+            E_all.append(E)
+            TM_all.append(tm)
+    finally:
+        ex.shutdown(cancel_futures=True)
+    _check_mass_invariant(res, lay)
+    _check_ranking(res, np.stack(E_all), lay, planted, e_tol=E_RANK_TOL)
+    return res
+
+
+@pytest.mark.timeout(900)
+def test_all_layers_long_video():
+    """65,664 tokens (1024 frames), 28 layers: evidence, non-visual mass and
+    the query rows' O and LSE on every layer; pooled scores and rankings."""
+    say("case config-4, all 28 layers")
+    _all_layers_query_rows(wl.get(4))
+
+
+@pytest.mark.timeout(900)
+def test_all_layers_ragged_batch():
+    """8 packed videos of 64-512 frames x 32 tokens, 28 layers: as above,
+    with one ranking per video."""
+    say("case config-5, all 28 layers")
+    _all_layers_query_rows(wl.get(5))
 
 
 def test_deterministic_bitwise():
