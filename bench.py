@@ -43,7 +43,8 @@ PEAK_HBM_GBS = 8000.0
 # Sources whose change invalidates the committed counter figures: the
 # attention kernel and the plan that orders its work (launch order decides
 # how much of the key/value traffic each XCD's L2 absorbs).
-TRAFFIC_SOURCES = ("attn.hip", "plan.cpp", "plan.h")
+TRAFFIC_SOURCES = ("attn.hip", "attn_pipe.hip", "attn_tiles.h", "plan.cpp",
+                   "plan.h")
 
 
 def traffic_source_sha():
@@ -59,7 +60,8 @@ def measured_traffic():
     """HBM bytes per attention launch from the committed counter summary,
     or None when the attention kernel or the plan changed since it was
     measured."""
-    summ = os.path.join(ROOT, "profiles", "attn_kernel_16k28L_hbm_counters.md")
+    summ = os.path.join(ROOT, "profiles",
+                        "attn_pipe_kernel_16k28L_hbm_counters.md")
     try:
         sha = traffic_source_sha()
         for line in open(summ):
@@ -67,6 +69,33 @@ def measured_traffic():
                 kv = dict(x.split("=") for x in line.split()[1:])
                 if kv["source_sha256"] == sha:
                     return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
+    except (OSError, KeyError, ValueError):
+        pass
+    return None
+
+
+def attention_kernel_name(w, args):
+    """The attention kernel the library launches for this run: the
+    pipelined kernel for bf16 inputs under the static rule without frame
+    cues, attn_kernel otherwise."""
+    if w.dtype == "bf16" and w.tau_p == 0 and not args.cues:
+        return f"attn_pipe_kernel<{w.d}>"
+    path = "Bf16Path" if w.dtype == "bf16" else "F32Path"
+    return f"attn_kernel<{path}<{w.d}>, {w.d}, {'true' if w.tau_p > 0 else 'false'}>"
+
+
+def measured_sq():
+    """MFMA busy, co-execution and VALU/MFMA ratio of the attention kernel
+    from the committed SQ counter summary, or None when the attention kernel
+    or the plan changed since it was measured."""
+    summ = os.path.join(ROOT, "profiles", "attn_pipe_kernel_16k28L_sq_counters.md")
+    try:
+        sha = traffic_source_sha()
+        for line in open(summ):
+            if line.startswith("sq_per_launch"):
+                kv = dict(x.split("=") for x in line.split()[1:])
+                if kv.pop("source_sha256") == sha:
+                    return {k: float(v) for k, v in kv.items()}
     except (OSError, KeyError, ValueError):
         pass
     return None
@@ -488,7 +517,12 @@ def main():
                      # counters cover the static-rule kernel without cues
                      "traffic": (measured_traffic() if args.config == 3 and
                                  w.tau_p == 0 and not args.cues else None),
-                     "kernel": "attn_kernel<Bf16Path<128>>",
+                     "kernel": attention_kernel_name(w, args),
+                     # SQ counters of the same kernel and workload (null when
+                     # stale or for another workload)
+                     "sq_counters": (measured_sq() if args.config == 3 and
+                                     w.tau_p == 0 and not args.cues
+                                     else None),
                      "flop_per_launch": flop_layer,
                      "avg_launch_ms": attn_ms,
                      "timed_launches": prof_attn["calls"]},
@@ -513,7 +547,7 @@ def main():
     if w.tau_p > 0:
         rec["config"]["tau_p"] = w.tau_p
         rec["config"]["sink_blocks"] = rec["config"]["window"] = None
-        rec["roofline"]["kernel"] = "attn_kernel<Bf16Path<128>, top-p>"
+
         rec["topp"] = {"computed_tile_pairs_per_layer": flop_layer / tile_flop,
                        "candidate_tile_pairs_per_layer":
                            float(w.hq * st["n_active_pairs"]),

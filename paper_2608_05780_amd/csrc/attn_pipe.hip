@@ -11,12 +11,11 @@
 //            registers by the previous iteration) between them;
 //   block 2  O^T += V(j)^T P(j)^T (16 MFMAs), with the exponentials of tile
 //            j+1's keys 0-31.
-// Each MFMA then has about two exponentials and two fused multiply-adds
-// beside it, which issue while it executes. Probabilities are rounded to
-// bf16 once, for the PV product, and every sum is taken over those rounded
-// values (v_dot2_f32_bf16 against (1, 1)): a row's normaliser and, for
-// query-token rows, its per-frame partial masses are exactly the weights
-// the output used.
+// Each MFMA then has about two exponentials, two fused multiply-adds and two
+// adds beside it, which issue while it executes. Probabilities are rounded
+// to bf16 for the PV product only; a row's normaliser and, for query-token
+// rows, its per-frame partial masses are fp32 sums of the fp32
+// probabilities, as in attn_kernel.
 //
 // The softmax reference of a row is the exact row max of its first tile and
 // never moves in this loop: no tile max, no rescale. A tile whose row sum
@@ -40,8 +39,6 @@
 
 namespace evisel {
 namespace {
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // The scalar arguments the kernel reads.
 struct PipeArgs {
@@ -71,16 +68,6 @@ struct Tile {
   int start, len, region, aux;
   bool act;   // some row of this wave's half attends to it
 };
-
-// Sum of the eight bf16 values of x (as fp32), added to acc.
-__device__ __forceinline__ float bsum8(const bf16x8& x, float acc) {
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{x[2 * i], x[2 * i + 1]}, one,
-                                          acc, false);
-  return acc;
-}
 
 // Instruction order requested from the scheduler (sched_group_barrier
 // masks: 0x008 MFMA, 0x100 LDS read, 0x002 VALU).
@@ -279,15 +266,21 @@ attn_pipe_kernel(const PipeArgs a) {
     sched_reads_ahead<KK, 1>();
   };
   // probabilities of one half against the reference, as two bf16 groups;
-  // query-token rows also sum them in fp32 per 8-key group (g4)
-  auto soft_half = [&](const f32x16& s, bf16x8& p0, bf16x8& p1, float mu) {
+  // returns their fp32 sum
+  auto soft_half = [&](const f32x16& s, bf16x8& p0, bf16x8& p1,
+                       float mu) -> float {
     f32x16 p;
+    float sum = 0.f;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) p[r] = exp2_(fmaf(s[r], c2, -mu));
+    for (int r = 0; r < 16; ++r) {
+      p[r] = exp2_(fmaf(s[r], c2, -mu));
+      sum += p[r];
+    }
     p0 = __builtin_convertvector(
         __builtin_shufflevector(p, p, 0, 1, 2, 3, 4, 5, 6, 7), bf16x8);
     p1 = __builtin_convertvector(
         __builtin_shufflevector(p, p, 8, 9, 10, 11, 12, 13, 14, 15), bf16x8);
+    return sum;
   };
   // O^T += V^T P^T over the tile at vt
   auto pv_tile = [&](const EV_LDS char* vt, const bf16x8 (&pb)[4]) {
@@ -434,22 +427,20 @@ attn_pipe_kernel(const PipeArgs a) {
     constexpr bool TXT = decltype(txt)::value;
     // Carried between iterations, for the tile in flight (tile j at the top
     // of iteration j): the logits of its keys 32-63 (s1), the bf16
-    // probabilities of its keys 0-31 (pb[0..1]) and their sum (visual rows:
-    // th, over the bf16 values; query-token rows: gh, fp32 per 8-key group).
+    // probabilities of its keys 0-31 (pb[0..1]) and their fp32 sum (th).
     // A tile that is not active for this wave's rows (half of a paired item)
     // takes its probabilities against +inf, so they are all 0 and its PV
     // product adds nothing; only a wave's first active tile needs a branch
     // (its row max sets the reference).
     f32x16 s0, s1;
     bf16x8 pb[4];
-    float th = 0.f;   // visual: bf16 sum; query tokens: fp32 sum (keys 0-31)
+    float th = 0.f;   // fp32 sum of the probabilities of keys 0-31
     bool started = false, bad = false;
     const float pinf = __builtin_inff();
 
     // keys 0-31 of a tile (logits in s0) to pb[0..1] and their sum
     auto start_half = [&](float mu) {
-      soft_half(s0, pb[0], pb[1], mu);
-      th = bsum8(pb[1], bsum8(pb[0], 0.f));
+      th = soft_half(s0, pb[0], pb[1], mu);
     };
     // a wave's first active tile: the exact row max of its logits (both
     // halves, masked) is the reference
@@ -462,16 +453,10 @@ attn_pipe_kernel(const PipeArgs a) {
       m_ref = mx == neg_inf() ? 0.f : mx * c2;
       started = true;
     };
-    // end of tile t once its keys 32-63 are in pb[2..3]
-    auto finish = [&](const Tile& t) {
-      float ts;
-      if (TXT) {
-        const float h1 = bsum8(pb[3], bsum8(pb[2], 0.f));
-        ts = th + h1;
-        if (t.act) text_tile_halves(t, th, h1);
-      } else {
-        ts = bsum8(pb[3], bsum8(pb[2], th));
-      }
+    // end of tile t once its keys 32-63 are in pb[2..3] (h1: their sum)
+    auto finish = [&](const Tile& t, float h1) {
+      const float ts = th + h1;
+      if (TXT && t.act) text_tile_halves(t, th, h1);
       bad = bad || __any(active && !(ts <= kFastBound));
       l_part += ts;
     };
@@ -523,7 +508,7 @@ attn_pipe_kernel(const PipeArgs a) {
         for (int kk = 0; kk < KK; ++kk)
           n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf.x[kk], n0,
                                                        0, 0, 0);
-        soft_half(s1, pb[2], pb[3], mu_c);
+        const float h1 = soft_half(s1, pb[2], pb[3], mu_c);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
           n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[KK + kk], qf.x[kk],
@@ -531,7 +516,7 @@ attn_pipe_kernel(const PipeArgs a) {
         sched_block1<KK, 40 / KK>();
         s0 = n0;
         s1 = n1;
-        finish(cur);
+        finish(cur, h1);
       }
       if (need_mask(nxt)) mask_half(s0, 0, nxt);
       if (!started && active && nxt.act) first_tile(nxt);
@@ -569,8 +554,7 @@ attn_pipe_kernel(const PipeArgs a) {
     {
       const Tile cur = tc;
       if (need_mask(cur)) mask_half(s1, 1, cur);
-      soft_half(s1, pb[2], pb[3], cur.act ? m_ref : pinf);
-      finish(cur);
+      finish(cur, soft_half(s1, pb[2], pb[3], cur.act ? m_ref : pinf));
       pv_tile(vb0 + (j & 1) * TB, pb);
     }
     // votes, in V0 (the O rows are staged in K0 and K1 afterwards): every
@@ -637,14 +621,9 @@ attn_pipe_kernel(const PipeArgs a) {
 
 }  // namespace
 
-// Off: the first launch of an earlier form of this kernel stopped with an
-// illegal-address fault whose cause has not been identified, so every call
-// takes attn_kernel until it has.
-constexpr bool kPipeEnabled = false;
-
 bool attention_pipe_supported(const DevPlan& p, const AttnCall& c) {
-  return kPipeEnabled && !c.fp32 && !p.topp && c.segv == nullptr &&
-         c.lse2v == nullptr && (c.d == 64 || c.d == 128);
+  return !c.fp32 && !p.topp && c.segv == nullptr && c.lse2v == nullptr &&
+         (c.d == 64 || c.d == 128);
 }
 
 hipError_t launch_attention_pipe(const DevPlan& p, const Workspace& w,

@@ -74,10 +74,15 @@ __device__ __forceinline__ int swz(int row) {
 // address is an input operand bound to m0 (the register the instruction
 // takes it from), so the compiler writes m0 itself and knows it holds that
 // value; it passes through readfirstlane because it is wave-uniform and m0
-// is a scalar register. The s_nop separates the m0 write from its use.
+// is a scalar register. The s_nop 4 gives the instruction five wait states
+// after whatever precedes it: a vector-memory instruction that reads an SGPR
+// written by a VALU instruction (v_readlane_b32, which the compiler uses to
+// restore spilled SGPRs such as gbase) needs five, and the compiler inserts
+// them only for memory instructions it knows about, not for inline assembly.
+// The same nop covers the one wait state between the m0 write and its use.
 __device__ __forceinline__ void lds_dma16(uint32_t lds, const char* gbase,
                                           uint32_t voff) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1"
                :
                : "v"(voff), "s"(gbase),
                  "{m0}"(__builtin_amdgcn_readfirstlane(lds))
