@@ -1,0 +1,142 @@
+"""Compiled-code check of the direct global -> LDS loads (CPU only: hipcc
+cross-compiles the attention sources for gfx950 to assembly).
+
+On gfx9 a vector-memory instruction that reads an SGPR written by a VALU
+instruction needs five wait states in between. The compiler inserts them
+for the memory instructions it emits itself, but the tile loads are inline
+assembly (global_load_lds_dwordx4 with a scalar base), whose operands the
+compiler may fill from spilled SGPRs with v_readlane_b32 right before the
+instruction. Without the wait states the load can take a stale base and
+address arbitrary memory. The loads therefore start with their own
+s_nop 4; this test scans every kernel of the attention sources and fails
+on any load whose SGPR base, or m0, was written by a VALU instruction fewer
+than five wait states earlier, or whose base is not in SGPRs at all."""
+import os
+import re
+import shutil
+import subprocess
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_05780_amd", "csrc")
+SOURCES = ["attn.hip", "attn_pipe.hip"]
+WAIT_STATES = 5
+
+
+def _hipcc():
+    for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc",
+              shutil.which("hipcc")):
+        if c and os.path.exists(c):
+            return c
+    return None
+
+
+def _sregs(tok):
+    m = re.fullmatch(r"s\[(\d+):(\d+)\]", tok)
+    if m:
+        return {f"s{i}" for i in range(int(m.group(1)), int(m.group(2)) + 1)}
+    m = re.fullmatch(r"s(\d+)", tok)
+    if m:
+        return {tok}
+    if tok in ("vcc", "vcc_lo", "vcc_hi", "m0"):
+        return {"vcc_lo", "vcc_hi"} if tok == "vcc" else {tok}
+    return set()
+
+
+def _valu_sgpr_defs(ins):
+    """SGPRs (and m0) a VALU instruction writes."""
+    op, *args = ins.replace(",", " ").split()
+    if not op.startswith("v_"):
+        return set()
+    out = set()
+    if op.startswith(("v_readlane", "v_readfirstlane")):
+        out |= _sregs(args[0])
+    elif op.startswith("v_cmp") and op.endswith("_e64"):
+        out |= _sregs(args[0])
+    elif op.startswith("v_cmp"):
+        out |= {"vcc_lo", "vcc_hi"}
+    elif ("_co_" in op or op.startswith(("v_mad_u64", "v_mad_i64",
+                                         "v_div_scale"))) and len(args) > 1:
+        out |= _sregs(args[1])
+    return out
+
+
+def scan(asm_text):
+    """(number of LDS-DMA loads, list of violations) of one .s file."""
+    n, bad = 0, []
+    hist = []   # (wait states, SGPRs written by VALU, text)
+    fn = "?"
+    for line in asm_text.split("\n"):
+        t = line.strip()
+        m = re.match(r"^(_Z\w+):", t)
+        if m:
+            fn, hist = m.group(1), []
+            continue
+        if not t or t.startswith((";", ".")) or t.endswith(":"):
+            continue
+        if t.startswith("global_load_lds"):
+            n += 1
+            base = t.replace(",", " ").split()[2]
+            uses = _sregs(base)
+            if not uses:
+                bad.append((fn, t, "base not in SGPRs"))
+            uses = uses | {"m0"}
+            ws = 0
+            for w, defs, txt in reversed(hist):
+                if ws >= WAIT_STATES:
+                    break
+                if defs & uses:
+                    bad.append((fn, t, f"{ws} wait states after {txt}"))
+                    break
+                ws += w
+        op = t.split()[0]
+        w = int(t.split()[1], 0) + 1 if op == "s_nop" else 1
+        hist.append((w, _valu_sgpr_defs(t), t))
+        hist = hist[-16:]
+    return n, bad
+
+
+def test_scanner_flags_the_hazard():
+    """The scanner itself: a load right after a spill reload is flagged,
+    the same load behind s_nop 4 is not."""
+    hazard = """_Zk:
+\tv_readlane_b32 s7, v227, 54
+\ts_mov_b32 m0, s33
+\ts_nop 0
+\tglobal_load_lds_dwordx4 v2, s[6:7]
+"""
+    n, bad = scan(hazard)
+    assert n == 1 and len(bad) == 1
+    n, bad = scan(hazard.replace("s_nop 0", "s_nop 4"))
+    assert n == 1 and not bad
+    n, bad = scan(hazard.replace("s[6:7]", "v[6:7]"))
+    assert bad and "SGPR" in bad[0][2]
+
+
+@pytest.mark.slow
+def test_lds_dma_operands_have_their_wait_states(tmp_path):
+    hipcc = _hipcc()
+    if hipcc is None:
+        pytest.skip("hipcc not available")
+
+    def compile_one(src):
+        out = tmp_path / (src + ".s")
+        cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17",
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+               "--cuda-device-only", "-S", os.path.join(CSRC, src),
+               "-o", str(out)]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-2000:]
+        return out.read_text()
+
+    with ThreadPoolExecutor(len(SOURCES)) as ex:
+        texts = list(ex.map(compile_one, SOURCES))
+    total = 0
+    for src, text in zip(SOURCES, texts):
+        n, bad = scan(text)
+        total += n
+        assert not bad, (src, bad[:5])
+    assert total > 500   # every attention kernel variant was scanned
