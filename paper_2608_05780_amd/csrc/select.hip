@@ -19,12 +19,14 @@
 //                largest t* whose tail mass F(t*) = sum_{e_j >= t*} e_j still
 //                reaches the threshold. t* is found by bisection over the
 //                bit patterns of the non-negative fp32 e_j (ordered like the
-//                values), stopping once a single candidate value is left.
-//                When several e_j equal t*, they are retained in ascending
-//                block order until the threshold is reached. Every sum runs
-//                in a fixed order, F is monotone in t, and the lanes of a row
-//                see identical reductions, so the result is bitwise
-//                reproducible.
+//                values), stopping once a single candidate value is left;
+//                after two passes over all entries, each lane copies the
+//                few entries still inside the bracket to its LDS slice and
+//                the remaining passes read only those. When several e_j
+//                equal t*, they are retained in ascending block order until
+//                the threshold is reached. Every sum runs in a fixed order
+//                and the lanes of a row see identical reductions, so the
+//                result is bitwise reproducible.
 // seg_fill_kernel  -inf into the per-(row, frame) partial masses before a
 //                top-p attention pass (tiles that no row of a work item
 //                retained are skipped and write nothing).
@@ -156,7 +158,17 @@ inline size_t sel_lds_bytes(int nh, int tpr, int W) {
 // LDS, entries [j0, j0 + cnt) of the row's history at my[0 .. cnt). Sets the
 // retained history bits in wrow (LDS, OR). Both variants compute the same
 // result; retain_row_regs keeps the lane's L <= kRegVals values in registers.
+//
+// The bisection keeps F(lo) >= thr > F(hi) with the counts clo, chi of the
+// entries >= lo, >= hi. Each lane also keeps a, its partial sum at the last
+// hi, and evaluates F(mid) as a plus its entries in [mid, hi) in index
+// order, summed over the row's lanes in a fixed tree. F is then a function
+// of (mid, hi, a) alone, whichever entries a pass visits, so the
+// register variant may stop scanning entries outside [lo, hi) once they are
+// few: it copies them, in order, into the lane's LDS slice and runs the
+// remaining passes over that list.
 constexpr int kRegVals = 36;
+constexpr int kFullPasses = 2;   // passes over every entry before the copy
 
 // Bits [j0, j0 + n) of a row from a lane's mask (n <= 64, j0 % 4 == 0).
 __device__ __forceinline__ void or_bits(uint32_t* wrow, int j0,
@@ -170,17 +182,61 @@ __device__ __forceinline__ void or_bits(uint32_t* wrow, int j0,
   if ((unsigned)hi) atomicOr(wrow + w0 + 2, (unsigned)hi);
 }
 
+// One bisection step from the lane's partial f = a + (its entries in
+// [mid, hi)) and their count k.
 template <int TPR>
-__device__ __forceinline__ void retain_row_regs(const float* my, int L,
-                                                int cnt, int nh, int j0,
-                                                float tau, int lane, int part,
+__device__ __forceinline__ void bisect_step(float f, int k, unsigned mid,
+                                            float thr, unsigned& lo,
+                                            unsigned& hi, int& clo, int& chi,
+                                            float& fhi, float& a) {
+  const float F = grp_sum<TPR>(f);
+  const int K = chi + grp_sumi<TPR>(k);          // entries >= mid
+  if (F >= thr) {
+    lo = mid;
+    clo = K;
+  } else {
+    hi = mid;
+    chi = K;
+    fhi = F;
+    a = f;
+  }
+}
+
+// Ties at lo (several entries with the bit pattern lo and F(lo + 1) < thr):
+// how many of them to take, in ascending block order, and how many of them
+// lie in this lane's lower-numbered neighbours.
+template <int TPR>
+__device__ __forceinline__ void tie_share(int mine, float fhi, float thr,
+                                          unsigned lo, int nt, int lane,
+                                          int part, int& take, int& rank) {
+  const float et = __uint_as_float(lo);
+  float cum = fhi;
+  take = 0;
+  while (take < nt && cum < thr) {
+    cum += et;
+    ++take;
+  }
+  rank = 0;
+  for (int q2 = 0; q2 < TPR; ++q2) {
+    const int o = __shfl(mine, lane - part + q2);
+    rank += q2 < part ? o : 0;
+  }
+}
+
+template <int TPR>
+__device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
+                                                int nh, int j0, float tau,
+                                                int lane, int part,
                                                 uint32_t* wrow) {
   constexpr int NCK = kRegVals / 4;
   const int nck = L >> 2;                         // uniform per work-group
   // Entries past the history read as -inf, so their e is +0; the cut t*
   // found below is never 0 (F at any key up to the smallest positive e is
   // the whole sum Z >= tau Z), so zeros are never retained or counted as
-  // ties, and no validity mask is needed after the load.
+  // ties, and no validity mask is needed after the load. (The empty asm
+  // keeps the compiler from hoisting the 36 entry tests out of the caller's
+  // row loop, where their lane masks would not fit in SGPRs.)
+  asm volatile("" : "+v"(cnt));
   float v[kRegVals];
 #pragma unroll
   for (int c = 0; c < NCK; ++c) {
@@ -202,70 +258,93 @@ __device__ __forceinline__ void retain_row_regs(const float* my, int L,
     v[i] = x;
     z += x;
     const unsigned kb = __float_as_uint(x);
-    kmin = min(kmin, kb ? kb : 0xFFFFFFFFu);
+    kmin = min(kmin, kb - 1u);                    // +0 wraps to the top
     kmax = max(kmax, kb);
   }
   z = grp_sum<TPR>(z);
-  kmin = grp_minu<TPR>(kmin);
+  kmin = grp_minu<TPR>(kmin) + 1u;
   kmax = grp_maxu<TPR>(kmax);
   const float thr = tau * z;
-  // F(lo) >= thr > F(hi); clo / chi count the entries >= lo / >= hi
   unsigned lo = kmin, hi = kmax + 1u;
   int clo = nh, chi = 0;
-  float fhi = 0.f;
-  while (hi - lo > 1u && clo - chi > 1) {
-    const unsigned mid = lo + ((hi - lo) >> 1);
-    float f = 0.f;
+  float fhi = 0.f, a = 0.f;
+  for (int it = 0; it < kFullPasses && hi - lo > 1u && clo - chi > 1; ++it) {
+    const unsigned mid = lo + ((hi - lo) >> 1), span = hi - mid;
+    float f = a;
     int k = 0;
 #pragma unroll
     for (int c = 0; c < NCK; ++c) {
       if (c < nck) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool in = __float_as_uint(v[4 * c + e]) >= mid;
+          const bool in = __float_as_uint(v[4 * c + e]) - mid < span;
           f += in ? v[4 * c + e] : 0.f;
           k += in;
         }
       }
     }
-    f = grp_sum<TPR>(f);
-    k = grp_sumi<TPR>(k);
-    if (f >= thr) {
-      lo = mid;
-      clo = k;
-    } else {
-      hi = mid;
-      chi = k;
-      fhi = f;
-    }
+    bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
   }
-  const bool tie = clo - chi > 1;
-  int take = 0, rank = 0;
-  if (tie) {
-    const float et = __uint_as_float(lo);
-    float cum = fhi;
-    const int nt = clo - chi;
-    while (take < nt && cum < thr) {
-      cum += et;
-      ++take;
+  if (hi - lo > 1u && clo - chi > 1) {
+    // the lane's entries in [lo, hi), in index order, to my[0 .. n), then
+    // zeros up to a multiple of 4 (n <= L, a multiple of 4; +0 lies below
+    // every lo). Each store lands at or below the entry's own slot.
+    const unsigned span = hi - lo;
+    int n = 0;
+#pragma unroll
+    for (int c = 0; c < NCK; ++c) {
+      if (c < nck) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          my[n] = v[4 * c + e];
+          n += __float_as_uint(v[4 * c + e]) - lo < span;
+        }
+      }
     }
+    const int n4 = (n + 3) & ~3;
+    for (int i = n; i < n4; ++i) my[i] = 0.f;
+    do {
+      const unsigned mid = lo + ((hi - lo) >> 1), sp = hi - mid;
+      float f = a;
+      int k = 0;
+      for (int i = 0; i < n4; i += 4) {
+        const f32x4 t = *(const f32x4*)(my + i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool in = __float_as_uint(t[e]) - mid < sp;
+          f += in ? t[e] : 0.f;
+          k += in;
+        }
+      }
+      bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
+    } while (hi - lo > 1u && clo - chi > 1);
+  }
+  if (clo - chi <= 1) {
+    // no tie: the entries >= lo
+    unsigned m0 = 0u, m1 = 0u;
+#pragma unroll
+    for (int i = 0; i < 32; ++i)
+      m0 |= __float_as_uint(v[i]) >= lo ? 1u << i : 0u;
+#pragma unroll
+    for (int i = 32; i < kRegVals; ++i)
+      m1 |= __float_as_uint(v[i]) >= lo ? 1u << (i - 32) : 0u;
+    or_bits(wrow, j0, ((unsigned long long)m1 << 32) | m0);
+  } else {
     int mine = 0;
 #pragma unroll
     for (int i = 0; i < kRegVals; ++i) mine += __float_as_uint(v[i]) == lo;
-    for (int q2 = 0; q2 < TPR; ++q2) {
-      const int o = __shfl(mine, lane - part + q2);
-      rank += q2 < part ? o : 0;
-    }
-  }
-  unsigned long long m = 0ull;
+    int take, rank;
+    tie_share<TPR>(mine, fhi, thr, lo, clo - chi, lane, part, take, rank);
+    unsigned long long m = 0ull;
 #pragma unroll
-  for (int i = 0; i < kRegVals; ++i) {
-    const unsigned kb = __float_as_uint(v[i]);
-    bool sel = kb >= lo;
-    if (tie && kb == lo) sel = rank++ < take;
-    m |= (unsigned long long)sel << i;
+    for (int i = 0; i < kRegVals; ++i) {
+      const unsigned kb = __float_as_uint(v[i]);
+      bool sel = kb > lo;
+      if (kb == lo) sel = rank++ < take;
+      m |= (unsigned long long)sel << i;
+    }
+    or_bits(wrow, j0, m);
   }
-  or_bits(wrow, j0, m);
 }
 
 template <int TPR>
@@ -287,65 +366,44 @@ __device__ __forceinline__ void retain_row_lds(float* my, int L, int cnt,
     f32x4 t = *(const f32x4*)(my + i);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const bool ok = i + e < cnt;
-      const float x = ok ? __builtin_amdgcn_exp2f(t[e] - mx) : 0.f;
+      const float x = i + e < cnt ? __builtin_amdgcn_exp2f(t[e] - mx) : 0.f;
       t[e] = x;
       z += x;
-      if (ok) {
-        kmin = min(kmin, __float_as_uint(x));
-        kmax = max(kmax, __float_as_uint(x));
-      }
+      const unsigned kb = __float_as_uint(x);
+      kmin = min(kmin, kb - 1u);
+      kmax = max(kmax, kb);
     }
     *(f32x4*)(my + i) = t;
   }
   z = grp_sum<TPR>(z);
-  kmin = grp_minu<TPR>(kmin);
+  kmin = grp_minu<TPR>(kmin) + 1u;
   kmax = grp_maxu<TPR>(kmax);
   const float thr = tau * z;
   unsigned lo = kmin, hi = kmax + 1u;
   int clo = nh, chi = 0;
-  float fhi = 0.f;
+  float fhi = 0.f, a = 0.f;
   while (hi - lo > 1u && clo - chi > 1) {
-    const unsigned mid = lo + ((hi - lo) >> 1);
-    float f = 0.f;
+    const unsigned mid = lo + ((hi - lo) >> 1), span = hi - mid;
+    float f = a;
     int k = 0;
 #pragma unroll 2
     for (int i = 0; i < L; i += 4) {
       const f32x4 t = *(const f32x4*)(my + i);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const bool in = __float_as_uint(t[e]) >= mid;
+        const bool in = __float_as_uint(t[e]) - mid < span;
         f += in ? t[e] : 0.f;
         k += in;
       }
     }
-    f = grp_sum<TPR>(f);
-    k = grp_sumi<TPR>(k);
-    if (f >= thr) {
-      lo = mid;
-      clo = k;
-    } else {
-      hi = mid;
-      chi = k;
-      fhi = f;
-    }
+    bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
   }
   const bool tie = clo - chi > 1;
   int take = 0, rank = 0;
   if (tie) {
-    const float et = __uint_as_float(lo);
-    float cum = fhi;
-    const int nt = clo - chi;
-    while (take < nt && cum < thr) {
-      cum += et;
-      ++take;
-    }
     int mine = 0;
     for (int i = 0; i < cnt; ++i) mine += __float_as_uint(my[i]) == lo;
-    for (int q2 = 0; q2 < TPR; ++q2) {
-      const int o = __shfl(mine, lane - part + q2);
-      rank += q2 < part ? o : 0;
-    }
+    tie_share<TPR>(mine, fhi, thr, lo, clo - chi, lane, part, take, rank);
   }
   // 32 entries at a time (j0 % 4 == 0, so a run covers at most 2 words)
   for (int i0 = 0; i0 < cnt; i0 += 32) {
