@@ -432,30 +432,35 @@ __device__ __forceinline__ void affinity_tiles(
   const int ntile = (nh + 31) / 32;
   const int rl = rg * 32 + l32;
   const bool rv = rl < rows && r0 + rl < qb.len;
-  const size_t qoff = ((size_t)(qb.start + r0 + rl) * pl.hq + h) * D;
+  // rows past the block read the block's first row; their affinities are
+  // never stored
+  const size_t qoff = ((size_t)(qb.start + (rv ? r0 + rl : 0)) * pl.hq + h) * D;
   if (!F32) {
     bf16x8 qf[D / 16];
     const __bf16* qs = (const __bf16*)q + qoff + 8 * g;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      bf16x8 z = {};
-      qf[kk] = rv ? *(const bf16x8*)(qs + 16 * kk) : z;
-    }
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qs + 16 * kk);
     const __bf16* kh0 =
         (const __bf16*)kbar + ((size_t)kvh * pl.nb + first) * D + 8 * g;
     const size_t lo_off = (size_t)pl.hkv * pl.nb * D;
     for (int t = ph; t < ntile; t += wpg) {
       const int jb = min(32 * t + l32, nh - 1);
       const __bf16* kh = kh0 + (size_t)jb * D;
+      // every operand load of the tile in flight before the first MFMA
+      bf16x8 ah[D / 16], al[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        ah[kk] = *(const bf16x8*)(kh + 16 * kk);
+        al[kk] = *(const bf16x8*)(kh + lo_off + 16 * kk);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       f32x16 acc = {};
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 ah = *(const bf16x8*)(kh + 16 * kk);
-        const bf16x8 al = *(const bf16x8*)(kh + lo_off + 16 * kk);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, qf[kk], acc, 0, 0,
-                                                      0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, qf[kk], acc, 0, 0,
-                                                      0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[kk], qf[kk], acc, 0,
+                                                      0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[kk], qf[kk], acc, 0,
+                                                      0, 0);
       }
       if (rv) {
 #pragma unroll
