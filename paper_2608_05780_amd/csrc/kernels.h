@@ -43,7 +43,7 @@ struct Workspace {
   float* pNV;    // [slots][64]     log2 partial mass on non-visual keys
   float* seg;    // [hq][segtot]    log2 partial mass per (query row, frame)
   // top-p retention (null for the static rule)
-  void* kbar;              // bf16: hi [hkv][nb][d] then lo; fp32: [hkv][nb][d]
+  void* kbar;              // bf16: hi [hkv][d/8][nb][8] then lo; fp32: [hkv][nb][d]
   uint32_t* rbits;         // [hq][nb][W][64] retained history per row
   uint32_t* ubits;         // [hq][nb][W]     union over the block's rows
   float* cpart;            // coarse evidence per-block partial sums

@@ -72,10 +72,12 @@ __global__ __launch_bounds__(D) void pool_kernel(const DevPlan pl,
       if (r0 + i < bd.len) s += x[i];
   }
   const float m = s / (float)bd.len;
-  const size_t o = ((size_t)kvh * pl.nb + b) * D + c;
   if (F32) {
-    ((float*)kbar)[o] = m;
+    ((float*)kbar)[((size_t)kvh * pl.nb + b) * D + c] = m;
   } else {
+    // d-chunk-major: the 8-element chunk c / 8 of every block is
+    // contiguous, so a 32-block MFMA operand load reads 512 bytes in a row
+    const size_t o = (((size_t)kvh * (D / 8) + c / 8) * pl.nb + b) * 8 + (c & 7);
     const __bf16 hi = (__bf16)m;
     const __bf16 lo = (__bf16)(m - (float)hi);
     ((__bf16*)kbar)[o] = hi;
@@ -440,18 +442,20 @@ __device__ __forceinline__ void affinity_tiles(
     const __bf16* qs = (const __bf16*)q + qoff + 8 * g;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qs + 16 * kk);
-    const __bf16* kh0 =
-        (const __bf16*)kbar + ((size_t)kvh * pl.nb + first) * D + 8 * g;
+    // chunk 2 kk + g of block first + jb (d-chunk-major layout)
+    const __bf16* kh0 = (const __bf16*)kbar +
+                        (((size_t)kvh * (D / 8) + g) * pl.nb + first) * 8;
     const size_t lo_off = (size_t)pl.hkv * pl.nb * D;
+    const size_t kk_step = (size_t)2 * pl.nb * 8;
     for (int t = ph; t < ntile; t += wpg) {
       const int jb = min(32 * t + l32, nh - 1);
-      const __bf16* kh = kh0 + (size_t)jb * D;
+      const __bf16* kh = kh0 + (size_t)jb * 8;
       // every operand load of the tile in flight before the first MFMA
       bf16x8 ah[D / 16], al[D / 16];
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        ah[kk] = *(const bf16x8*)(kh + 16 * kk);
-        al[kk] = *(const bf16x8*)(kh + lo_off + 16 * kk);
+        ah[kk] = *(const bf16x8*)(kh + kk * kk_step);
+        al[kk] = *(const bf16x8*)(kh + lo_off + kk * kk_step);
       }
       __builtin_amdgcn_sched_barrier(0);
       f32x16 acc = {};
