@@ -151,9 +151,16 @@ __host__ __device__ inline int sel_per_thread(int nh, int tpr) {
 __host__ __device__ inline int sel_stride(int nh, int tpr) {
   return tpr * sel_per_thread(nh, tpr) + 4;
 }
-inline size_t sel_lds_bytes(int nh, int tpr, int W) {
-  return (size_t)(kSelThreads / tpr) * sel_stride(nh, tpr) * 4 +
-         (size_t)64 * W * 4;
+// LDS floats ahead of the per-row bit words: a pass's affinities
+// [rows][stride] for the longest history, which also hold the pass's query
+// rows ([rows][d + 8] bf16) while they are read into registers.
+__host__ __device__ inline int sel_region0(int nh_max, int tpr, int d) {
+  const int rpw = kSelThreads / tpr;
+  const int ev = rpw * sel_stride(nh_max, tpr), qs = rpw * (d + 8) / 2;
+  return ev > qs ? ev : qs;
+}
+inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
+  return (size_t)(sel_region0(nh_max, tpr, d) + 64 * W) * 4;
 }
 
 // Retention of one row whose TPR lanes hold e-candidates g_j (log2 units) in
@@ -429,7 +436,8 @@ template <bool F32, int D>
 __device__ __forceinline__ void affinity_tiles(
     const DevPlan& pl, const void* kbar, const void* q, float scale_log2,
     const BlockDesc& qb, int h, int kvh, int first, int nh, int r0, int rows,
-    int rg, int ph, int wpg, float* ev, int stride, int lane) {
+    int rg, int ph, int wpg, float* ev, int stride, int lane,
+    const __bf16* qs = nullptr) {
   const int l32 = lane & 31, g = lane >> 5;
   const int ntile = (nh + 31) / 32;
   const int rl = rg * 32 + l32;
@@ -439,9 +447,20 @@ __device__ __forceinline__ void affinity_tiles(
   const size_t qoff = ((size_t)(qb.start + (rv ? r0 + rl : 0)) * pl.hq + h) * D;
   if (!F32) {
     bf16x8 qf[D / 16];
-    const __bf16* qs = (const __bf16*)q + qoff + 8 * g;
+    if (qs) {
+      // rows staged in LDS by the whole work-group ([rows][D + 8]); every
+      // wave has its operands before the first affinity overwrites them
+      const __bf16* qr = qs + min(rl, rows - 1) * (D + 8) + 8 * g;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qs + 16 * kk);
+      for (int kk = 0; kk < D / 16; ++kk)
+        qf[kk] = *(const bf16x8*)(qr + 16 * kk);
+      __syncthreads();
+    } else {
+      const __bf16* qg = (const __bf16*)q + qoff + 8 * g;
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk)
+        qf[kk] = *(const bf16x8*)(qg + 16 * kk);
+    }
     // chunk 2 kk + g of block first + jb (d-chunk-major layout)
     const __bf16* kh0 = (const __bf16*)kbar +
                         (((size_t)kvh * (D / 8) + g) * pl.nb + first) * 8;
@@ -450,21 +469,27 @@ __device__ __forceinline__ void affinity_tiles(
     for (int t = ph; t < ntile; t += wpg) {
       const int jb = min(32 * t + l32, nh - 1);
       const __bf16* kh = kh0 + (size_t)jb * 8;
-      // every operand load of the tile in flight before the first MFMA
-      bf16x8 ah[D / 16], al[D / 16];
-#pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        ah[kk] = *(const bf16x8*)(kh + kk * kk_step);
-        al[kk] = *(const bf16x8*)(kh + lo_off + kk * kk_step);
-      }
-      __builtin_amdgcn_sched_barrier(0);
+      // the tile's operand loads in two halves of D / 32 chunks each
       f32x16 acc = {};
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[kk], qf[kk], acc, 0,
-                                                      0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[kk], qf[kk], acc, 0,
-                                                      0, 0);
+      for (int hf = 0; hf < 2; ++hf) {
+        constexpr int HK = D / 32;
+        bf16x8 ah[HK], al[HK];
+#pragma unroll
+        for (int u = 0; u < HK; ++u) {
+          const int kk = hf * HK + u;
+          ah[u] = *(const bf16x8*)(kh + kk * kk_step);
+          al[u] = *(const bf16x8*)(kh + lo_off + kk * kk_step);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < HK; ++u) {
+          const int kk = hf * HK + u;
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[u], qf[kk], acc, 0,
+                                                        0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[u], qf[kk], acc, 0,
+                                                        0, 0);
+        }
       }
       if (rv) {
 #pragma unroll
@@ -536,7 +561,8 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
   const int L = sel_per_thread(nh, TPR);
   const int stride = sel_stride(nh, TPR);
   float* const ev = dyn;                                  // [RPW][stride]
-  uint32_t* const wb = (uint32_t*)(dyn + RPW * stride);   // [64][W]
+  uint32_t* const wb =                                    // [64][W]
+      (uint32_t*)(dyn + sel_region0(max(pl.hmax, 1), TPR, D));
   for (int i = tid; i < 64 * W; i += kSelThreads) wb[i] = 0u;
 
   const int kvh = h / (pl.hq / pl.hkv);
@@ -545,8 +571,34 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
 
   for (int r0 = 0; r0 < qb.len; r0 += RPW) {
     // ---- affinities of rows r0 .. r0 + RPW - 1 against the history ----
+    __bf16* qs = nullptr;
+    if (!F32) {
+      // the pass's query rows to LDS in whole 16-byte chunks (rows past
+      // the block repeat its last row; their affinities are never stored)
+      qs = (__bf16*)dyn;
+      constexpr int CPR = D / 8;
+      constexpr int NST = (RPW * CPR + kSelThreads - 1) / kSelThreads;
+      bf16x8 st[NST];
+#pragma unroll
+      for (int u = 0; u < NST; ++u) {
+        const int i = min(tid + u * kSelThreads, RPW * CPR - 1);
+        const int row = i / CPR, c = i - row * CPR;
+        const int tok = qb.start + min(r0 + row, qb.len - 1);
+        st[u] = *(const bf16x8*)((const __bf16*)sc.q +
+                                 ((size_t)tok * pl.hq + h) * D + 8 * c);
+      }
+#pragma unroll
+      for (int u = 0; u < NST; ++u) {
+        const int i = tid + u * kSelThreads;
+        if (i < RPW * CPR) {
+          const int row = i / CPR, c = i - row * CPR;
+          *(bf16x8*)(qs + row * (D + 8) + 8 * c) = st[u];
+        }
+      }
+      __syncthreads();
+    }
     affinity_tiles<F32, D>(pl, ws.kbar, sc.q, sc.scale_log2, qb, h, kvh, first,
-                           nh, r0, RPW, rg, ph, WPG, ev, stride, lane);
+                           nh, r0, RPW, rg, ph, WPG, ev, stride, lane, qs);
     __syncthreads();
 
     // ---- retention of each row (TPR lanes per row) ----
@@ -810,14 +862,14 @@ hipError_t launch_sel_d(const DevPlan& p, const Workspace& w,
   int pick = -1;
   for (int i = 0; i < 3 && pick < 0; ++i)
     if (sel_per_thread(nh_max, tprs[i]) <= kRegVals &&
-        sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsTwoPerCu)
+        sel_lds_bytes(nh_max, tprs[i], p.W, D) <= kSelLdsTwoPerCu)
       pick = i;
   for (int i = 0; i < 3 && pick < 0; ++i)
-    if (sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsTwoPerCu) pick = i;
+    if (sel_lds_bytes(nh_max, tprs[i], p.W, D) <= kSelLdsTwoPerCu) pick = i;
   for (int i = 0; i < 3 && pick < 0; ++i)
-    if (sel_lds_bytes(nh_max, tprs[i], p.W) <= kSelLdsMax) pick = i;
+    if (sel_lds_bytes(nh_max, tprs[i], p.W, D) <= kSelLdsMax) pick = i;
   if (pick < 0) return hipErrorInvalidValue;
-  const size_t lds = sel_lds_bytes(nh_max, tprs[pick], p.W);
+  const size_t lds = sel_lds_bytes(nh_max, tprs[pick], p.W, D);
   if (pick == 0) return launch_sel<F32, D, 4>(p, w, c, lds, s);
   if (pick == 1) return launch_sel<F32, D, 8>(p, w, c, lds, s);
   return launch_sel<F32, D, 16>(p, w, c, lds, s);
@@ -826,7 +878,7 @@ hipError_t launch_sel_d(const DevPlan& p, const Workspace& w,
 }  // namespace
 
 size_t select_lds_need(int nh_max, int W) {
-  return sel_lds_bytes(nh_max, 16, W);
+  return sel_lds_bytes(nh_max, 16, W, 128);
 }
 
 hipError_t launch_select(const DevPlan& p, const Workspace& w,
