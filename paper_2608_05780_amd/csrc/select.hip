@@ -255,20 +255,32 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
     for (int e = 0; e < 4; ++e)
       v[4 * c + e] = 4 * c + e < cnt ? t[e] : neg_inf();
   }
+  // (chunks c >= nck hold no entries: skipped, and +0 from here on)
   float mx = neg_inf();
 #pragma unroll
-  for (int i = 0; i < kRegVals; ++i) mx = fmaxf(mx, v[i]);
+  for (int c = 0; c < NCK; ++c)
+    if (c < nck)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, v[4 * c + e]);
   mx = grp_max<TPR>(mx);
   float z = 0.f;
   unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
-  for (int i = 0; i < kRegVals; ++i) {
-    const float x = __builtin_amdgcn_exp2f(v[i] - mx);
-    v[i] = x;
-    z += x;
-    const unsigned kb = __float_as_uint(x);
-    kmin = min(kmin, kb - 1u);                    // +0 wraps to the top
-    kmax = max(kmax, kb);
+  for (int c = 0; c < NCK; ++c) {
+    if (c < nck) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = __builtin_amdgcn_exp2f(v[4 * c + e] - mx);
+        v[4 * c + e] = x;
+        z += x;
+        const unsigned kb = __float_as_uint(x);
+        kmin = min(kmin, kb - 1u);                // +0 wraps to the top
+        kmax = max(kmax, kb);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * c + e] = 0.f;
+    }
   }
   z = grp_sum<TPR>(z);
   kmin = grp_minu<TPR>(kmin) + 1u;
@@ -332,11 +344,19 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
     // no tie: the entries >= lo
     unsigned m0 = 0u, m1 = 0u;
 #pragma unroll
-    for (int i = 0; i < 32; ++i)
-      m0 |= __float_as_uint(v[i]) >= lo ? 1u << i : 0u;
+    for (int c = 0; c < NCK; ++c) {
+      if (c < nck) {
 #pragma unroll
-    for (int i = 32; i < kRegVals; ++i)
-      m1 |= __float_as_uint(v[i]) >= lo ? 1u << (i - 32) : 0u;
+        for (int e = 0; e < 4; ++e) {
+          const int i = 4 * c + e;
+          const bool sel = __float_as_uint(v[i]) >= lo;
+          if (i < 32)
+            m0 |= sel ? 1u << i : 0u;
+          else
+            m1 |= sel ? 1u << (i - 32) : 0u;
+        }
+      }
+    }
     or_bits(wrow, j0, ((unsigned long long)m1 << 32) | m0);
   } else {
     int mine = 0;
