@@ -544,7 +544,12 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
   using T = typename P::T;
   constexpr int TB = kTile * P::RC * 16;
   constexpr int RB = 2 * 64 * 32 * 4;              // wave-pair hand-off
-  __shared__ __attribute__((aligned(1024))) char smem[TB > RB ? TB : RB];
+  // bf16: the key tile, then both heads' query rows of the current pair
+  // (staged like a key tile); fp32 rows are read from global memory
+  constexpr bool kStageQ = sizeof(T) == 2;
+  constexpr int SM = kStageQ ? 3 * TB : (TB > RB ? TB : RB);
+  static_assert(SM >= RB, "hand-off buffer");
+  __shared__ __attribute__((aligned(1024))) char smem[SM];
   EV_LDS char* kt = (EV_LDS char*)smem;
   const BlockDesc qb = pl.blocks[blockIdx.x];
   if (qb.region != kVis) return;
@@ -587,26 +592,56 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
         acc[c][r] += ok ? exp2_(fmaf(s[c][r], c2, -l2)) : 0.f;
       }
   };
-  typename P::QFrag qa, qb2;
-  float la = 0.f, lb = 0.f;
-  fetch(qa, la, head(0));
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();                                 // K tile in LDS
-  for (int pi = 0; pi < npair; pi += 2) {
-    fetch(qb2, lb, head(pi + 1));
-    accumulate(qa, la, head(pi));
-    fetch(qa, la, head(pi + 2));
-    accumulate(qb2, lb, head(pi + 1));
+  if constexpr (kStageQ) {
+    // pair pi's query rows: head 2 pi + s of the group to slot s, in whole
+    // 16-byte chunks of each row; wave w reads slot w / 2
+    EV_LDS char* qs = kt + TB;
+    TileLoader<T, D, kSwzK> qload;
+    qload.init(pl.hq, wave, lane);
+    auto stage = [&](int pi) {
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+        if (pi < npair && 2 * pi + s2 < group)
+          qload.issue(qs + s2 * TB, (const T*)ac.q, qb.start, qb.len,
+                      kvh * group + 2 * pi + s2, wave);
+    };
+    stage(0);
+    for (int pi = 0; pi < npair; ++pi) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();                             // K tile, pair pi's rows
+      const int h = head(pi);
+      typename P::QFrag qf;
+      float l2 = 0.f;
+      if (h >= 0) {
+        P::load_q_lds(qf, qs + (wave >> 1) * TB, qrow, g);
+        l2 = qvalid ? ws.lse2v[(size_t)h * pl.S + qpos] : 0.f;
+      }
+      __syncthreads();                             // the slots may refill
+      stage(pi + 1);
+      accumulate(qf, l2, h);
+    }
+  } else {
+    typename P::QFrag qa, qb2;
+    float la = 0.f, lb = 0.f;
+    fetch(qa, la, head(0));
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();                               // K tile in LDS
+    for (int pi = 0; pi < npair; pi += 2) {
+      fetch(qb2, lb, head(pi + 1));
+      accumulate(qa, la, head(pi));
+      fetch(qa, la, head(pi + 2));
+      accumulate(qb2, lb, head(pi + 1));
+    }
   }
-  // waves 2-3 hand their sums to waves 0-1 through LDS
+  // waves 2-3 hand their sums to waves 0-1 through LDS (lane-contiguous)
   __syncthreads();
-  float* red = (float*)smem;                       // [2][64 lanes][32]
+  float* red = (float*)smem;                       // [2][32][64 lanes]
   if (wave >= 2) {
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        red[((wave & 1) * 64 + lane) * 32 + 16 * c + r] = acc[c][r];
+        red[((wave & 1) * 32 + 16 * c + r) * 64 + lane] = acc[c][r];
   }
   __syncthreads();
   if (wave >= 2 || !qvalid) return;
@@ -620,7 +655,7 @@ void intra_kernel(const DevPlan pl, const Workspace ws, const AttnCall ac) {
       const int kl = 32 * c + 8 * (r >> 2) + 4 * g + (r & 3);
       if (kl / Nv != fr || kl >= qb.len) continue;
       dst[kl % Nv] =
-          acc[c][r] + red[((wave & 1) * 64 + lane) * 32 + 16 * c + r];
+          acc[c][r] + red[((wave & 1) * 32 + 16 * c + r) * 64 + lane];
     }
 }
 

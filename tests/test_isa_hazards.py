@@ -40,8 +40,10 @@ SGPR_SPILL_BUDGET = {
     "attn_kernelINS0_7F32PathILi128EEELi128ELb1": 91,
     "attn_kernelINS0_7F32PathILi64EEELi64ELb0": 78,
     "attn_kernelINS0_7F32PathILi64EEELi64ELb1": 90,
-    "intra_kernelINS0_8Bf16PathILi128": 66, "intra_kernelINS0_8Bf16PathILi64": 67,
-    "intra_kernelINS0_7F32PathILi128": 65, "intra_kernelINS0_7F32PathILi64": 67,
+    # the intra-frame kernel stages each head pair's query rows with the
+    # tile loader (bf16), which holds the loader's offsets across the loop
+    "intra_kernelINS0_8Bf16PathILi128": 74, "intra_kernelINS0_8Bf16PathILi64": 74,
+    "intra_kernelINS0_7F32PathILi128": 68, "intra_kernelINS0_7F32PathILi64": 69,
     "intra_reduce_kernel": 0,
 }
 
