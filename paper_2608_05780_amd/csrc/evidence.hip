@@ -305,6 +305,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(
 // pair gets the mean over heads and frame a's rows.
 constexpr int kPairWaves = 4;
 
+constexpr int kPairHeads = 8;
+
 __global__ __launch_bounds__(64 * kPairWaves) void frame_pairs_kernel(
     const DevPlan pl, const Workspace ws, float* __restrict__ out) {
   const int lane = threadIdx.x & 63;
@@ -319,25 +321,35 @@ __global__ __launch_bounds__(64 * kPairWaves) void frame_pairs_kernel(
   const int group = pl.hq / pl.hkv;
   const bool rv = lane < pl.Nv;
   const int row = fp.roff + (rv ? lane : 0);
+  // heads in groups of kPairHeads: the group's loads go out together, the
+  // sum still runs in head order
   float acc = 0.f;
-  for (int h = 0; h < pl.hq; ++h) {
-    bool done = always;
-    if (!always) {
-      const int g0 = (h / group) * group;
-      const int h0 = g0 + ((h - g0) / kHeadsPerItem) * kHeadsPerItem;
-      const int nh = min(kHeadsPerItem, g0 + group - h0);
-      unsigned wd = 0u;
-      for (int i = 0; i < nh; ++i)
-        wd |= ws.ubits[((size_t)(h0 + i) * pl.nb + fp.qblock) * pl.W +
-                       (loc >> 5)];
-      done = (wd >> (loc & 31)) & 1u;
+  for (int hb = 0; hb < pl.hq; hb += kPairHeads) {
+    float sv[kPairHeads], l2[kPairHeads];
+    bool dn[kPairHeads];
+#pragma unroll
+    for (int u = 0; u < kPairHeads; ++u) {
+      const int h = hb + u;
+      bool done = always;
+      if (!always && h < pl.hq) {
+        const int g0 = (h / group) * group;
+        const int h0 = g0 + ((h - g0) / kHeadsPerItem) * kHeadsPerItem;
+        const int nh = min(kHeadsPerItem, g0 + group - h0);
+        unsigned wd = 0u;
+        for (int i = 0; i < nh; ++i)
+          wd |= ws.ubits[((size_t)(h0 + i) * pl.nb + fp.qblock) * pl.W +
+                         (loc >> 5)];
+        done = (wd >> (loc & 31)) & 1u;
+      }
+      dn[u] = done && rv && h < pl.hq;
+      sv[u] = dn[u] ? ws.segv[(((size_t)h * pl.nnz + fp.pos) * fpt +
+                                fp.koff) * 64 + row]
+                    : 0.f;
+      l2[u] = dn[u] ? ws.lse2v[(size_t)h * pl.S + qb.start + row] : 0.f;
     }
-    if (done && rv) {
-      const float sv =
-          ws.segv[(((size_t)h * pl.nnz + fp.pos) * fpt + fp.koff) * 64 + row];
-      const float l2 = ws.lse2v[(size_t)h * pl.S + qb.start + row];
-      acc += exp2_(sv - l2);
-    }
+#pragma unroll
+    for (int u = 0; u < kPairHeads; ++u)
+      if (dn[u]) acc += exp2_(sv[u] - l2[u]);
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
