@@ -264,7 +264,7 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
       for (int e = 0; e < 4; ++e) mx = fmaxf(mx, v[4 * c + e]);
   mx = grp_max<TPR>(mx);
   float z = 0.f;
-  unsigned kmin = 0xFFFFFFFFu, kmax = 0u;
+  unsigned kmin = 0xFFFFFFFFu;
 #pragma unroll
   for (int c = 0; c < NCK; ++c) {
     if (c < nck) {
@@ -273,9 +273,7 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
         const float x = __builtin_amdgcn_exp2f(v[4 * c + e] - mx);
         v[4 * c + e] = x;
         z += x;
-        const unsigned kb = __float_as_uint(x);
-        kmin = min(kmin, kb - 1u);                // +0 wraps to the top
-        kmax = max(kmax, kb);
+        kmin = min(kmin, __float_as_uint(x) - 1u);  // +0 wraps to the top
       }
     } else {
 #pragma unroll
@@ -284,15 +282,17 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
   }
   z = grp_sum<TPR>(z);
   kmin = grp_minu<TPR>(kmin) + 1u;
-  kmax = grp_maxu<TPR>(kmax);
   const float thr = tau * z;
-  unsigned lo = kmin, hi = kmax + 1u;
+  // the row's largest e is exp2(0) = 1 exactly
+  unsigned lo = kmin, hi = __float_as_uint(1.f) + 1u;
   int clo = nh, chi = 0;
   float fhi = 0.f, a = 0.f;
-  for (int it = 0; it < kFullPasses && hi - lo > 1u && clo - chi > 1; ++it) {
+  // The full passes count nothing: a bracket that already holds a single
+  // entry only narrows around it, which keeps the same retained set. The
+  // count of entries inside the bracket is taken when they are copied.
+  for (int it = 0; it < kFullPasses && hi - lo > 1u; ++it) {
     const unsigned mid = lo + ((hi - lo) >> 1), span = hi - mid;
     float f = a;
-    int k = 0;
 #pragma unroll
     for (int c = 0; c < NCK; ++c) {
       if (c < nck) {
@@ -300,13 +300,28 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
         for (int e = 0; e < 4; ++e) {
           const bool in = __float_as_uint(v[4 * c + e]) - mid < span;
           f += in ? v[4 * c + e] : 0.f;
-          k += in;
         }
       }
     }
-    bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
+    const float F = grp_sum<TPR>(f);
+    if (F >= thr) {
+      lo = mid;
+    } else {
+      hi = mid;
+      fhi = F;
+      a = f;
+    }
   }
-  if (hi - lo > 1u && clo - chi > 1) {
+  if (hi - lo <= 1u) {
+    // [lo, hi) = {lo}: its entries (every lane of the row sees the count)
+    int mine = 0;
+#pragma unroll
+    for (int c = 0; c < NCK; ++c)
+      if (c < nck)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mine += __float_as_uint(v[4 * c + e]) == lo;
+    clo = grp_sumi<TPR>(mine);
+  } else {
     // the lane's entries in [lo, hi), in index order, to my[0 .. n), then
     // zeros up to a multiple of 4 (n <= L, a multiple of 4; +0 lies below
     // every lo). Each store lands at or below the entry's own slot.
@@ -324,7 +339,10 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
     }
     const int n4 = (n + 3) & ~3;
     for (int i = n; i < n4; ++i) my[i] = 0.f;
-    do {
+    // from here clo - chi counts the row's entries inside the bracket
+    clo = grp_sumi<TPR>(n);
+    chi = 0;
+    while (hi - lo > 1u && clo - chi > 1) {
       const unsigned mid = lo + ((hi - lo) >> 1), sp = hi - mid;
       float f = a;
       int k = 0;
@@ -338,7 +356,7 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
         }
       }
       bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
-    } while (hi - lo > 1u && clo - chi > 1);
+    }
   }
   if (clo - chi <= 1) {
     // no tie: the entries >= lo
