@@ -124,13 +124,15 @@ def _classify(q, k, lay, blk, rows, keep_o, keep_g, info, scale, tau, d):
     return match, amb
 
 
-def _run_case(w, rows_budget=None, seed=0, layers=None):
+def _run_case(w, rows_budget=None, seed=0, layers=None, transform=None):
     ev = pytest.ev
     lay = _layout(w, seed)
     blk = topp.Blocks(lay, w.block)
     layers = layers if layers is not None else list(range(w.n_layers))
     keeps = {}
     inputs = {l: wl.gen_layer(w, l, seed) for l in layers}
+    if transform is not None:
+        inputs = {l: transform(x, lay, blk) for l, x in inputs.items()}
     res = run_gpu(ev, w, layers, seed, layer_inputs=lambda l: inputs[l])
     for j, l in enumerate(layers):
         q, k, v = inputs[l].as_f64()
@@ -279,6 +281,49 @@ def test_topp_uniform_affinity_ties():
             np.testing.assert_array_equal(ko[h, j], want)
         checked += 1
     assert checked > 1000
+
+
+def _dup_key_blocks(x, lay, blk):
+    """Every third visual block takes block 1's keys (bit for bit), so those
+    blocks share one mean key and every row sees a run of exactly equal
+    affinities, which some rows' cuts fall inside."""
+    k = x.k.copy()
+    starts = [s for s in range(lay.S) if lay.frame[s] >= 0 and
+              (s == 0 or lay.frame[s - 1] != lay.frame[s])]
+    src = starts[1]
+    for j, s in enumerate(starts):
+        if j >= 3 and j % 3 == 0 and s + 64 <= lay.S and \
+                (lay.frame[s:s + 64] >= 0).all():
+            k[s:s + 64] = k[src:src + 64]
+    return wl.Layer(q=x.q, k=k, v=x.v, u=x.u)
+
+
+def _scale_queries(x, lay, blk, f=200.0):
+    """Queries scaled so that a row's affinities span a few hundred log2
+    units: most probabilities underflow to +0 in fp32 and rows keep one or
+    two blocks."""
+    q = wl.bf16_bits(wl.bf16_bits_to_f32(x.q) * np.float32(f))
+    return wl.Layer(q=q, k=x.k, v=x.v, u=x.u)
+
+
+def test_topp_equal_affinity_runs():
+    w = _small("dup-keys", tokens_per_frame=64, n_frames=(150,),
+               n_text=(64,), n_sys=(0,), tau_p=TAU)
+    say("case duplicated key blocks")
+    _, keeps = _run_case(w, rows_budget=512, transform=_dup_key_blocks)
+    # equal probabilities sit inside the rounding margin, but the rule that
+    # takes them in block order is exact: every row keeps the oracle's set
+    ref, kg, _, _ = keeps[0]
+    np.testing.assert_array_equal(kg, ref["keep"])
+
+
+def test_topp_underflowing_probabilities():
+    w = _small("scaled-q", tokens_per_frame=64, n_frames=(120,),
+               n_text=(64,), n_sys=(2,), tau_p=TAU)
+    say("case queries x200")
+    _, keeps = _run_case(w, rows_budget=512, transform=_scale_queries)
+    ref, kg, _, _ = keeps[0]
+    np.testing.assert_array_equal(kg, ref["keep"])
 
 
 def test_topp_skips_tiles_and_is_deterministic():
