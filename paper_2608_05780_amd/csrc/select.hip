@@ -7,12 +7,16 @@
 //                token order divided by the block length. For bf16 inputs
 //                kbar is kept as two bf16 values, hi = RNE(kbar) and
 //                lo = RNE(kbar - hi), so the affinity can run on bf16 MFMA
-//                while kbar keeps about 16 significant bits.
+//                while kbar keeps about 16 significant bits; both arrays are
+//                d-chunk-major ([kv head][d / 8][block][8]), so the 32
+//                blocks of one MFMA operand load are contiguous.
 // select_kernel  one work-group per (query block, query head). The block's
 //                rows share their history (local blocks 0 .. nh-1 of the
-//                video). Affinities g = q . kbar * scale * log2(e) come from
-//                32x32x16 bf16 MFMA, hi and lo accumulated into one fp32
-//                tile (fp32 inputs: 32x32x2 f32 MFMA), and are staged in LDS,
+//                video). Each pass's query rows are staged in LDS once per
+//                work-group (bf16). Affinities g = q . kbar * scale *
+//                log2(e) come from 32x32x16 bf16 MFMA, hi and lo accumulated
+//                into one fp32 tile (fp32 inputs: 32x32x2 f32 MFMA), and are
+//                staged in LDS,
 //                each row owned by TPR consecutive lanes (TPR/4 quads). Per
 //                row: e_j = exp2(g_j - max), Z = sum e_j, threshold
 //                tau * Z. The retained set is {j : e_j >= t*} for the
@@ -168,10 +172,11 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // retained history bits in wrow (LDS, OR). Both variants compute the same
 // result; retain_row_regs keeps the lane's L <= kRegVals values in registers.
 //
-// The bisection keeps F(lo) >= thr > F(hi) with the counts clo, chi of the
-// entries >= lo, >= hi. Each lane also keeps a, its partial sum at the last
-// hi, and evaluates F(mid) as a plus its entries in [mid, hi) in index
-// order, summed over the row's lanes in a fixed tree. F is then a function
+// The bisection keeps F(lo) >= thr > F(hi), and clo - chi counts the
+// entries inside [lo, hi) (the register variant takes that count only when
+// it copies them). Each lane also keeps a, its partial sum at the last hi,
+// and evaluates F(mid) as a plus its entries in [mid, hi) in index order,
+// summed over the row's lanes in a fixed tree. F is then a function
 // of (mid, hi, a) alone, whichever entries a pass visits, so the
 // register variant may stop scanning entries outside [lo, hi) once they are
 // few: it copies them, in order, into the lane's LDS slice and runs the
