@@ -160,6 +160,31 @@ def oracle_query_rows(w: wl.Workload, seed: int, qt, k, v):
     return E, tm, O, LSE
 
 
+def oracle_topp_query_rows(w: wl.Workload, seed: int, qt, k, v):
+    """The oracle's top-p retention of one layer's query rows (``keep``,
+    ``info``), their evidence and non-visual mass, the mean keys the
+    retention used, and the rows' q (float64). ``qt`` holds q of those rows
+    only; k and v are whole (bf16 bit patterns or fp32). Runs in a worker
+    process: it imports neither torch nor the HIP library."""
+    from oracle import topp
+    from oracle.layout import Layout
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    lay = Layout(ns, nf, nt, w.tokens_per_frame)
+    blk = topp.Blocks(lay, w.block)
+    if qt.dtype == np.uint16:
+        cv = lambda a: wl.bf16_bits_to_f32(a).astype(np.float64)
+    else:
+        cv = lambda a: a.astype(np.float64)
+    txt = lay.text_rows()
+    q = np.zeros((lay.S,) + qt.shape[1:])
+    q[txt] = cv(qt)
+    k64, v64 = cv(k), cv(v)
+    keep, info = topp.select(q, k64, lay, blk, w.tau_p, w.softmax_scale, txt)
+    E, tm, _, _ = topp.evidence(q, k64, v64, lay, blk, keep, txt,
+                                w.softmax_scale)
+    return keep, info, E, tm, topp.mean_keys(k64, blk), q[txt]
+
+
 def _limit_threads(n):
     from threadpoolctl import threadpool_limits
     threadpool_limits(n)

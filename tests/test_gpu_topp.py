@@ -76,12 +76,15 @@ def _keep_of_rows(ev, rb, mask, blk, rows, max_count):
     return keep
 
 
-def _classify(q, k, lay, blk, rows, keep_o, keep_g, info, scale, tau, d):
+def _classify(q, k, lay, blk, rows, keep_o, keep_g, info, scale, tau, d,
+              kbar=None):
     """(match [Hq, R], ambiguous [Hq, R]); asserts that every mismatch is
-    ambiguous and still a valid top-p set."""
-    hq, hkv = q.shape[1], k.shape[1]
+    ambiguous and still a valid top-p set. ``kbar``: the oracle's mean keys
+    when ``k`` is not at hand."""
+    if kbar is None:
+        kbar = topp.mean_keys(k, blk)
+    hq, hkv = q.shape[1], kbar.shape[1]
     grp = hq // hkv
-    kbar = topp.mean_keys(k, blk)
     nh = info["nh"]
     match = (keep_o == keep_g).all(axis=2)
     amb = np.zeros_like(match)
@@ -379,6 +382,89 @@ def test_topp_config5_ragged_batch():
     w = wl.get(5, tau_p=TAU)
     say("case config-5 top-p, layer 0")
     _run_case(w, rows_budget=512, layers=[0])
+
+
+@pytest.mark.timeout(900)
+def test_topp_config3_all_layers_query_rows():
+    """All 28 layers of the bench workload under top-p: every query row's
+    retention against the oracle (differences only inside the rounding
+    margin), the evidence per (head, frame) on the frames no disagreeing row
+    touches, and the per-video ranking of the 28-layer pooled score. The
+    oracle runs in worker processes, fed the layer the GPU ran."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    import torch
+    from gpu_harness import oracle_topp_query_rows, _limit_threads
+    from test_gpu_parity import _check_ranking
+    w = wl.get(3, tau_p=TAU)
+    seed = 0
+    ev = pytest.ev
+    lay = _layout(w, seed)
+    blk = topp.Blocks(lay, w.block)
+    txt = lay.text_rows()
+    ns, nf, nt = wl.layout_arrays(w, seed)
+    # a mask of its own for the per-layer retention bits
+    mask = ev.build_block_mask(nf, nt, w.tokens_per_frame, w.block,
+                               w.sink_blocks, w.window, w.hq, w.hkv,
+                               n_sys=ns, tau_p=w.tau_p)
+    st = mask.stats
+    rb = torch.empty((w.hq, st["n_blocks"], st["hist_words"], 64),
+                     dtype=torch.int32, device="cuda")
+    ub = torch.empty((w.hq, st["n_blocks"], st["hist_words"]),
+                     dtype=torch.int32, device="cuda")
+    ws = torch.empty(ev.sparse_prefill_workspace(mask, w.d),
+                     dtype=torch.uint8, device="cuda")
+    _, core, _ = wl.plant_table(w, seed)
+    planted = [int(((core >= f0) & (core < f0 + F)).sum())
+               for f0, F in zip(lay.frame0, lay.n_frames)]
+    ks = [int(F) for F in lay.n_frames]
+    cache, futs, kept = {}, {}, {}
+    ex = cf.ProcessPoolExecutor(3, mp_context=mp.get_context("spawn"),
+                                initializer=_limit_threads, initargs=(5,))
+
+    def layer_inputs(l):
+        cache.clear()
+        cache[l] = wl.gen_layer(w, l, seed)
+        return cache[l]
+
+    def on_layer(j, l, out, lse):
+        x = cache[l]
+        futs[j] = ex.submit(oracle_topp_query_rows, w, seed, x.q[txt], x.k,
+                            x.v)
+        q, k, _ = to_device(x, w, torch)
+        ev.select_blocks(mask, q, k, rb, ub, ws, softmax_scale=w.softmax_scale)
+        torch.cuda.synchronize()
+        kept[j] = _keep_of_rows(ev, rb.cpu().numpy(), mask, blk, txt,
+                                blk.max_count)
+
+    try:
+        layers = list(range(w.n_layers))
+        res = run_gpu(ev, w, layers, seed, k_per_video=ks, keep_o=False,
+                      layer_inputs=layer_inputs, on_layer=on_layer)
+        E_ref_all, n_differ = [], 0
+        for j in layers:
+            keep, info, E_ref, tm_ref, kbar, q_txt = futs[j].result()
+            qf = np.zeros((lay.S, w.hq, w.d))
+            qf[txt] = q_txt
+            mt, _ = _classify(qf, None, lay, blk, txt, keep, kept[j], info,
+                              w.softmax_scale, w.tau_p, w.d, kbar=kbar)
+            okf = np.ones((w.hq, lay.T), bool)
+            for h, jj in zip(*np.nonzero(~mt)):
+                i = txt[jj]
+                for b in np.nonzero(kept[j][h, jj] != keep[h, jj])[0]:
+                    fr = lay.frame[blk.tokens(lay.seq[i], int(b))]
+                    okf[h, fr[fr >= 0]] = False
+            e_err = np.abs(res.E[j] - E_ref)[okf].max()
+            say(f"  layer {j}: E {e_err:.2e} "
+                f"({int((~mt).sum())} (head, row) pairs differ)")
+            assert e_err <= E_TOL
+            if mt.all():
+                assert np.abs(res.text_mass[j] - tm_ref).max() <= E_TOL
+            n_differ += int((~mt).sum())
+            E_ref_all.append(E_ref)
+    finally:
+        ex.shutdown(cancel_futures=True)
+    _check_ranking(res, np.stack(E_ref_all), lay, planted)
 
 
 def test_topp_config3_two_layers():
