@@ -169,18 +169,21 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 
 // Retention of one row whose TPR lanes hold e-candidates g_j (log2 units) in
 // LDS, entries [j0, j0 + cnt) of the row's history at my[0 .. cnt). Sets the
-// retained history bits in wrow (LDS, OR). Both variants compute the same
-// result; retain_row_regs keeps the lane's L <= kRegVals values in registers.
+// retained history bits in wrow (LDS, OR). retain_row_regs keeps the lane's
+// L <= kRegVals values in registers, retain_row_lds streams them from LDS.
+// Both find the same cut except where a tail sum F lies within its fp32
+// rounding of the threshold (they associate the sums differently).
 //
 // The bisection keeps F(lo) >= thr > F(hi), and clo - chi counts the
 // entries inside [lo, hi) (the register variant takes that count only when
-// it copies them). Each lane also keeps a, its partial sum at the last hi,
-// and evaluates F(mid) as a plus its entries in [mid, hi) in index order,
-// summed over the row's lanes in a fixed tree. F is then a function
-// of (mid, hi, a) alone, whichever entries a pass visits, so the
-// register variant may stop scanning entries outside [lo, hi) once they are
-// few: it copies them, in order, into the lane's LDS slice and runs the
-// remaining passes over that list.
+// it copies them). Each lane keeps a, its partial sum of the entries at or
+// above hi, and evaluates F(mid) as a plus its entries in [mid, hi) in
+// index order, summed over the row's lanes in a fixed tree. The register
+// variant runs two such passes over all its entries, then copies the few
+// entries still inside [lo, hi), in order, into the lane's LDS slice and
+// runs the remaining passes over that list, with a frozen at the copy (the
+// list holds no entry at or above that hi, so an entry counts towards
+// F(mid) when it is >= mid: one compare).
 constexpr int kRegVals = 36;
 constexpr int kFullPasses = 2;   // passes over every entry before the copy
 
@@ -344,23 +347,36 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
     }
     const int n4 = (n + 3) & ~3;
     for (int i = n; i < n4; ++i) my[i] = 0.f;
-    // from here clo - chi counts the row's entries inside the bracket
+    // From here F(mid) is a plus the lane's list entries >= mid, with a kept
+    // at its value for the bracket that was copied: the list holds no entry
+    // at or above that bracket's hi, and entries below lo lie below every
+    // later mid, so one compare per entry tests it. clo and chi count the
+    // list entries >= lo and >= hi.
     clo = grp_sumi<TPR>(n);
     chi = 0;
     while (hi - lo > 1u && clo - chi > 1) {
-      const unsigned mid = lo + ((hi - lo) >> 1), sp = hi - mid;
+      const unsigned mid = lo + ((hi - lo) >> 1);
       float f = a;
       int k = 0;
       for (int i = 0; i < n4; i += 4) {
         const f32x4 t = *(const f32x4*)(my + i);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool in = __float_as_uint(t[e]) - mid < sp;
+          const bool in = __float_as_uint(t[e]) >= mid;
           f += in ? t[e] : 0.f;
           k += in;
         }
       }
-      bisect_step<TPR>(f, k, mid, thr, lo, hi, clo, chi, fhi, a);
+      const float F = grp_sum<TPR>(f);
+      const int K = grp_sumi<TPR>(k);
+      if (F >= thr) {
+        lo = mid;
+        clo = K;
+      } else {
+        hi = mid;
+        chi = K;
+        fhi = F;
+      }
     }
   }
   if (clo - chi <= 1) {
