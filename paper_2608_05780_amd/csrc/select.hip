@@ -177,13 +177,15 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // The bisection keeps F(lo) >= thr > F(hi), and clo - chi counts the
 // entries inside [lo, hi) (the register variant takes that count only when
 // it copies them). Each lane keeps a, its partial sum of the entries at or
-// above hi, and evaluates F(mid) as a plus its entries in [mid, hi) in
-// index order, summed over the row's lanes in a fixed tree. The register
-// variant runs two such passes over all its entries, then copies the few
-// entries still inside [lo, hi), in order, into the lane's LDS slice and
-// runs the remaining passes over that list, with a frozen at the copy (the
-// list holds no entry at or above that hi, so an entry counts towards
-// F(mid) when it is >= mid: one compare).
+// above hi; the lanes' partials of F(mid) are summed over the row in a
+// fixed tree. The LDS variant takes a lane's partial as a plus its entries
+// in [mid, hi) in index order. The register variant runs two passes over
+// all its entries, each partial the sum of the lane's entries >= mid in
+// index order, then copies the few entries still inside [lo, hi), in order,
+// into the lane's LDS slice and runs the remaining passes over that list,
+// each partial a plus the list entries >= mid, with a frozen at the copy
+// (the list holds nothing at or above that hi, and entries below lo lie
+// below every later mid). Every entry test is then one compare.
 constexpr int kRegVals = 36;
 constexpr int kFullPasses = 2;   // passes over every entry before the copy
 
@@ -241,27 +243,23 @@ __device__ __forceinline__ void tie_share(int mine, float fhi, float thr,
 }
 
 template <int TPR>
-__device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
-                                                int nh, int j0, float tau,
-                                                int lane, int part,
-                                                uint32_t* wrow) {
+__device__ __forceinline__ void retain_row_regs(float* my, int L, int nh,
+                                                int j0, float tau, int lane,
+                                                int part, uint32_t* wrow) {
   constexpr int NCK = kRegVals / 4;
   const int nck = L >> 2;                         // uniform per work-group
-  // Entries past the history read as -inf, so their e is +0; the cut t*
-  // found below is never 0 (F at any key up to the smallest positive e is
-  // the whole sum Z >= tau Z), so zeros are never retained or counted as
-  // ties, and no validity mask is needed after the load. (The empty asm
-  // keeps the compiler from hoisting the 36 entry tests out of the caller's
-  // row loop, where their lane masks would not fit in SGPRs.)
-  asm volatile("" : "+v"(cnt));
+  // Entries past the history hold -inf (the affinity pass writes the row
+  // up to TPR * L), so their e is +0; the cut t* found below is never 0 (F
+  // at any key up to the smallest positive e is the whole sum Z >= tau Z),
+  // so zeros are never retained or counted as ties, and no validity mask
+  // is needed.
   float v[kRegVals];
 #pragma unroll
   for (int c = 0; c < NCK; ++c) {
     f32x4 t = {};
     if (c < nck) t = *(const f32x4*)(my + 4 * c);
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      v[4 * c + e] = 4 * c + e < cnt ? t[e] : neg_inf();
+    for (int e = 0; e < 4; ++e) v[4 * c + e] = t[e];
   }
   // (chunks c >= nck hold no entries: skipped, and +0 from here on)
   float mx = neg_inf();
@@ -299,14 +297,14 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
   // entry only narrows around it, which keeps the same retained set. The
   // count of entries inside the bracket is taken when they are copied.
   for (int it = 0; it < kFullPasses && hi - lo > 1u; ++it) {
-    const unsigned mid = lo + ((hi - lo) >> 1), span = hi - mid;
-    float f = a;
+    const unsigned mid = lo + ((hi - lo) >> 1);
+    float f = 0.f;   // all of the lane's entries >= mid
 #pragma unroll
     for (int c = 0; c < NCK; ++c) {
       if (c < nck) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool in = __float_as_uint(v[4 * c + e]) - mid < span;
+          const bool in = __float_as_uint(v[4 * c + e]) >= mid;
           f += in ? v[4 * c + e] : 0.f;
         }
       }
@@ -347,11 +345,8 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int cnt,
     }
     const int n4 = (n + 3) & ~3;
     for (int i = n; i < n4; ++i) my[i] = 0.f;
-    // From here F(mid) is a plus the lane's list entries >= mid, with a kept
-    // at its value for the bracket that was copied: the list holds no entry
-    // at or above that bracket's hi, and entries below lo lie below every
-    // later mid, so one compare per entry tests it. clo and chi count the
-    // list entries >= lo and >= hi.
+    // from here a lane's partial is a (frozen) plus its list entries >= mid;
+    // clo and chi count the list entries >= lo and >= hi
     clo = grp_sumi<TPR>(n);
     chi = 0;
     while (hi - lo > 1u && clo - chi > 1) {
@@ -488,17 +483,18 @@ __device__ __forceinline__ void retain_row_lds(float* my, int L, int cnt,
 
 // Affinities g = q . kbar * scale * log2(e) of rows r0 + rl (rl < rows) of
 // query block qb, head h, against its history blocks j < nh (global block
-// first + j), written to ev[rl * stride + j]. A wave takes the 32-row group
-// rg and every wpg-th 32-block tile from ph: S^T = Kbar Q^T on bf16 MFMA
-// with kbar = hi + lo accumulated into one fp32 tile (fp32: 32x32x2 MFMA).
+// first + j), written to ev[rl * stride + j]; columns nh <= j < ncols
+// (ncols <= stride) get -inf. A wave takes the 32-row group rg and every
+// wpg-th 32-column tile from ph: S^T = Kbar Q^T on bf16 MFMA with kbar =
+// hi + lo accumulated into one fp32 tile (fp32: 32x32x2 MFMA).
 template <bool F32, int D>
 __device__ __forceinline__ void affinity_tiles(
     const DevPlan& pl, const void* kbar, const void* q, float scale_log2,
-    const BlockDesc& qb, int h, int kvh, int first, int nh, int r0, int rows,
-    int rg, int ph, int wpg, float* ev, int stride, int lane,
-    const __bf16* qs = nullptr) {
+    const BlockDesc& qb, int h, int kvh, int first, int nh, int ncols,
+    int r0, int rows, int rg, int ph, int wpg, float* ev, int stride,
+    int lane, const __bf16* qs = nullptr) {
   const int l32 = lane & 31, g = lane >> 5;
-  const int ntile = (nh + 31) / 32;
+  const int ntile = (ncols + 31) / 32;
   const int rl = rg * 32 + l32;
   const bool rv = rl < rows && r0 + rl < qb.len;
   // rows past the block read the block's first row; their affinities are
@@ -554,7 +550,8 @@ __device__ __forceinline__ void affinity_tiles(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (j < nh) ev[rl * stride + j] = acc[r] * scale_log2;
+          if (j < ncols)
+            ev[rl * stride + j] = j < nh ? acc[r] * scale_log2 : neg_inf();
         }
       }
     }
@@ -586,7 +583,8 @@ __device__ __forceinline__ void affinity_tiles(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (j < nh) ev[rl * stride + j] = acc[r] * scale_log2;
+          if (j < ncols)
+            ev[rl * stride + j] = j < nh ? acc[r] * scale_log2 : neg_inf();
         }
       }
     }
@@ -657,7 +655,8 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
       __syncthreads();
     }
     affinity_tiles<F32, D>(pl, ws.kbar, sc.q, sc.scale_log2, qb, h, kvh, first,
-                           nh, r0, RPW, rg, ph, WPG, ev, stride, lane, qs);
+                           nh, TPR * L, r0, RPW, rg, ph, WPG, ev, stride, lane,
+                           qs);
     __syncthreads();
 
     // ---- retention of each row (TPR lanes per row) ----
@@ -670,7 +669,7 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
         float* const my = ev + rr * stride + j0;
         uint32_t* const wrow = wb + row * W;
         if (L <= kRegVals)
-          retain_row_regs<TPR>(my, L, cnt, nh, j0, sc.tau, lane, part, wrow);
+          retain_row_regs<TPR>(my, L, nh, j0, sc.tau, lane, part, wrow);
         else
           retain_row_lds<TPR>(my, L, cnt, nh, j0, sc.tau, lane, part, wrow);
       }
@@ -811,7 +810,7 @@ __global__ __launch_bounds__(kSelThreads) void coarse_kernel(
   const SeqDesc sq = pl.seqs[tt.seq];
   const int nsys = (sq.vis0 - sq.tok0 + kTile64 - 1) / kTile64;
   affinity_tiles<F32, D>(pl, ws.kbar, sc.q, sc.scale_log2, qb, h, kvh, first,
-                         nh, r0, RPW, 0, wave, 4, ev, stride, lane);
+                         nh, nh, r0, RPW, 0, wave, 4, ev, stride, lane);
   float mw, lw;
   exact_part<F32, D>(pl, sc, qb, qbid, h, kvh, first - nsys, nsys, r0, wave,
                      lane, mw, lw);
