@@ -364,6 +364,19 @@ def test_topp_long_history_streams_from_lds():
     _run_case(w, rows_budget=256)
 
 
+def test_topp_register_rows_of_sixteen_lanes():
+    # 340 visual blocks (d = 64): a row's share of the longest history fits
+    # the registers only at 16 lanes per row (24 entries each). Rows whose
+    # history holds 321-340 blocks (every query row among them) also get a
+    # whole 32-column tile of -inf padding past the end of their affinity
+    # row, which the register variant then loads as zero probabilities.
+    w = _small("sixteen-lanes", d=64, hq=2, hkv=1, tokens_per_frame=64,
+               n_frames=(340,), n_text=(40,), n_sys=(6,), tau_p=TAU,
+               key_struct=(1.0, 1.0, 0.9))
+    say("case sixteen lanes per row, register variant")
+    _run_case(w, rows_budget=256)
+
+
 def test_topp_config2_layer():
     w = wl.get(2, tau_p=TAU)
     say("case config-2 top-p")
