@@ -10,7 +10,8 @@
 //                while kbar keeps about 16 significant bits; both arrays are
 //                d-chunk-major ([kv head][d / 8][block][8]), so the 32
 //                blocks of one MFMA operand load are contiguous.
-// select_kernel  one work-group per (query block, query head). The block's
+// select_kernel  one work-group per (query block, query head), launched
+//                longest history first (see the kernel). The block's
 //                rows share their history (local blocks 0 .. nh-1 of the
 //                video). Each pass's query rows are staged in LDS once per
 //                work-group (bf16). Affinities g = q . kbar * scale *
@@ -602,7 +603,13 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
   constexpr int NRG = RPW >= 32 ? RPW / 32 : 1;   // 32-row MFMA groups
   constexpr int WPG = 4 / NRG;                    // waves per row group
   extern __shared__ __attribute__((aligned(16))) float dyn[];
-  const int qbid = blockIdx.x, h = blockIdx.y;
+  // one-dimensional grid, heads fastest, query blocks from the last: in a
+  // video the history grows with the block index, so the longest
+  // work-groups start first and the shortest fill the tail, and all heads
+  // of one block (which read whole token rows of q between them) run
+  // together
+  const int qbid = pl.nb - 1 - (int)blockIdx.x / pl.hq;
+  const int h = (int)blockIdx.x % pl.hq;
   const BlockDesc qb = pl.blocks[qbid];
   const int nh = pl.blk_local[qbid];              // |H|; -1 for system rows
   const int W = pl.W;
@@ -906,7 +913,7 @@ hipError_t launch_sel(const DevPlan& p, const Workspace& w, const SelCall& c,
         (int)lds);
     if (e != hipSuccess) return e;
   }
-  fn<<<dim3(p.nb, p.hq), dim3(kSelThreads), lds, s>>>(p, w, c);
+  fn<<<dim3(p.nb * p.hq), dim3(kSelThreads), lds, s>>>(p, w, c);
   return hipGetLastError();
 }
 
