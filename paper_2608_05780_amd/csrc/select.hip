@@ -482,6 +482,27 @@ __device__ __forceinline__ void retain_row_lds(float* my, int L, int cnt,
   }
 }
 
+// One 32x32 affinity tile's column share of a lane (row er of ev): columns
+// 32 t + 8 (r / 4) + 4 g + r % 4 for r < 16. A tile wholly inside the
+// history (the usual case, uniform over the wave) stores them unchecked.
+__device__ __forceinline__ void store_affinities(const f32x16& acc, float sc,
+                                                 float* er, int t, int g,
+                                                 int nh, int ncols, bool rv) {
+  if (!rv) return;
+  float* const e0 = er + 32 * t + 4 * g;
+  if (32 * t + 32 <= nh) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) e0[8 * (r >> 2) + (r & 3)] = acc[r] * sc;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+      if (j < ncols) e0[8 * (r >> 2) + (r & 3)] = j < nh ? acc[r] * sc
+                                                        : neg_inf();
+    }
+  }
+}
+
 // Affinities g = q . kbar * scale * log2(e) of rows r0 + rl (rl < rows) of
 // query block qb, head h, against its history blocks j < nh (global block
 // first + j), written to ev[rl * stride + j]; columns nh <= j < ncols
@@ -547,14 +568,7 @@ __device__ __forceinline__ void affinity_tiles(
                                                         0, 0);
         }
       }
-      if (rv) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (j < ncols)
-            ev[rl * stride + j] = j < nh ? acc[r] * scale_log2 : neg_inf();
-        }
-      }
+      store_affinities(acc, scale_log2, ev + rl * stride, t, g, nh, ncols, rv);
     }
   } else {
     float qf[D / 2];
@@ -580,14 +594,7 @@ __device__ __forceinline__ void affinity_tiles(
           acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], qf[4 * u + e], acc,
                                                      0, 0, 0);
       }
-      if (rv) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (j < ncols)
-            ev[rl * stride + j] = j < nh ? acc[r] * scale_log2 : neg_inf();
-        }
-      }
+      store_affinities(acc, scale_log2, ev + rl * stride, t, g, nh, ncols, rv);
     }
   }
 }
