@@ -62,18 +62,19 @@ __global__ __launch_bounds__(D) void pool_kernel(const DevPlan pl,
   if (bd.region == kSys) return;
   const size_t rs = (size_t)pl.hkv * D;
   const size_t base = ((size_t)bd.start * pl.hkv + kvh) * D + c;
-  // 16 loads in flight, then their sum in token order
+  // a whole 64-token block's loads in flight (one round trip), then their
+  // sum in token order
   float s = 0.f;
-  for (int r0 = 0; r0 < bd.len; r0 += 16) {
-    float x[16];
+  for (int r0 = 0; r0 < bd.len; r0 += kTile64) {
+    float x[kTile64];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < kTile64; ++i) {
       const int r = min(r0 + i, bd.len - 1);
       x[i] = F32 ? ((const float*)k)[base + r * rs]
                  : (float)((const __bf16*)k)[base + r * rs];
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
+    for (int i = 0; i < kTile64; ++i)
       if (r0 + i < bd.len) s += x[i];
   }
   const float m = s / (float)bd.len;
