@@ -25,7 +25,7 @@
 //                reaches the threshold. t* is found by bisection over the
 //                bit patterns of the non-negative fp32 e_j (ordered like the
 //                values), stopping once a single candidate value is left;
-//                after two passes over all entries, each lane copies the
+//                after four passes over all entries, each lane copies the
 //                few entries still inside the bracket to its LDS slice and
 //                the remaining passes read only those. When several e_j
 //                equal t*, they are retained in ascending block order until
@@ -181,7 +181,7 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // it copies them). Each lane keeps a, its partial sum of the entries at or
 // above hi; the lanes' partials of F(mid) are summed over the row in a
 // fixed tree. The LDS variant takes a lane's partial as a plus its entries
-// in [mid, hi) in index order. The register variant runs two passes over
+// in [mid, hi) in index order. The register variant runs four passes over
 // all its entries, each partial the sum of the lane's entries >= mid in
 // index order, then copies the few entries still inside [lo, hi), in order,
 // into the lane's LDS slice and runs the remaining passes over that list,
@@ -189,7 +189,11 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // (the list holds nothing at or above that hi, and entries below lo lie
 // below every later mid). Every entry test is then one compare.
 constexpr int kRegVals = 36;
-constexpr int kFullPasses = 2;   // passes over every entry before the copy
+// Passes over every entry before the copy: a full pass costs three VALU
+// instructions per entry, a pass over the copied list four and a half per
+// entry of the wave's longest list, so narrowing the lists first pays up to
+// four passes on rows of a few hundred near-uniform block affinities.
+constexpr int kFullPasses = 4;
 
 // Bits [j0, j0 + n) of a row from a lane's mask (n <= 64, j0 % 4 == 0).
 __device__ __forceinline__ void or_bits(uint32_t* wrow, int j0,
