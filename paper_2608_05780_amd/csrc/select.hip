@@ -172,7 +172,8 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // Retention of one row whose TPR lanes hold e-candidates g_j (log2 units) in
 // LDS, entries [j0, j0 + cnt) of the row's history at my[0 .. cnt). Sets the
 // retained history bits in wrow (LDS, OR). retain_row_regs keeps the lane's
-// L <= kRegVals values in registers, retain_row_lds streams them from LDS.
+// L <= RV values in registers (RV = kRegVals, or kRegValsLong for the long
+// form), retain_row_lds streams them from LDS.
 // Both find the same cut except where a tail sum F lies within its fp32
 // rounding of the threshold (they associate the sums differently).
 //
@@ -189,6 +190,7 @@ inline size_t sel_lds_bytes(int nh_max, int tpr, int W, int d) {
 // (the list holds nothing at or above that hi, and entries below lo lie
 // below every later mid). Every entry test is then one compare.
 constexpr int kRegVals = 36;
+constexpr int kRegValsLong = 72;   // the long form, 16 lanes per row
 // Passes over every entry before the copy: a full pass costs three VALU
 // instructions per entry, a pass over the copied list four and a half per
 // entry of the wave's longest list, so narrowing the lists first pays up to
@@ -205,6 +207,18 @@ __device__ __forceinline__ void or_bits(uint32_t* wrow, int j0,
   if ((unsigned)lo) atomicOr(wrow + w0, (unsigned)lo);
   if ((unsigned)(lo >> 32)) atomicOr(wrow + w0 + 1, (unsigned)(lo >> 32));
   if ((unsigned)hi) atomicOr(wrow + w0 + 2, (unsigned)hi);
+}
+// The same from NW 32-bit words (bit i of the lane's mask in word i / 32).
+template <int NW>
+__device__ __forceinline__ void or_bits_w(uint32_t* wrow, int j0,
+                                          const unsigned (&m)[NW]) {
+  const int w0 = j0 >> 5, off = j0 & 31;
+#pragma unroll
+  for (int k = 0; k <= NW; ++k) {
+    const unsigned cur = k < NW ? m[k] << off : 0u;
+    const unsigned prev = k > 0 && off ? m[k - 1] >> (32 - off) : 0u;
+    if (cur | prev) atomicOr(wrow + w0 + k, cur | prev);
+  }
 }
 
 // One bisection step from the lane's partial f = a + (its entries in
@@ -248,18 +262,19 @@ __device__ __forceinline__ void tie_share(int mine, float fhi, float thr,
   }
 }
 
-template <int TPR>
+template <int TPR, int RV>
 __device__ __forceinline__ void retain_row_regs(float* my, int L, int nh,
                                                 int j0, float tau, int lane,
                                                 int part, uint32_t* wrow) {
-  constexpr int NCK = kRegVals / 4;
+  constexpr int NCK = RV / 4;
+  constexpr int NW = (RV + 31) / 32;   // mask words
   const int nck = L >> 2;                         // uniform per work-group
   // Entries past the history hold -inf (the affinity pass writes the row
   // up to TPR * L), so their e is +0; the cut t* found below is never 0 (F
   // at any key up to the smallest positive e is the whole sum Z >= tau Z),
   // so zeros are never retained or counted as ties, and no validity mask
   // is needed.
-  float v[kRegVals];
+  float v[RV];
 #pragma unroll
   for (int c = 0; c < NCK; ++c) {
     f32x4 t = {};
@@ -380,9 +395,11 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int nh,
       }
     }
   }
+  unsigned mw[NW];
+#pragma unroll
+  for (int k = 0; k < NW; ++k) mw[k] = 0u;
   if (clo - chi <= 1) {
     // no tie: the entries >= lo
-    unsigned m0 = 0u, m1 = 0u;
 #pragma unroll
     for (int c = 0; c < NCK; ++c) {
       if (c < nck) {
@@ -390,30 +407,25 @@ __device__ __forceinline__ void retain_row_regs(float* my, int L, int nh,
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * c + e;
           const bool sel = __float_as_uint(v[i]) >= lo;
-          if (i < 32)
-            m0 |= sel ? 1u << i : 0u;
-          else
-            m1 |= sel ? 1u << (i - 32) : 0u;
+          mw[i >> 5] |= sel ? 1u << (i & 31) : 0u;
         }
       }
     }
-    or_bits(wrow, j0, ((unsigned long long)m1 << 32) | m0);
   } else {
     int mine = 0;
 #pragma unroll
-    for (int i = 0; i < kRegVals; ++i) mine += __float_as_uint(v[i]) == lo;
+    for (int i = 0; i < RV; ++i) mine += __float_as_uint(v[i]) == lo;
     int take, rank;
     tie_share<TPR>(mine, fhi, thr, lo, clo - chi, lane, part, take, rank);
-    unsigned long long m = 0ull;
 #pragma unroll
-    for (int i = 0; i < kRegVals; ++i) {
+    for (int i = 0; i < RV; ++i) {
       const unsigned kb = __float_as_uint(v[i]);
       bool sel = kb > lo;
       if (kb == lo) sel = rank++ < take;
-      m |= (unsigned long long)sel << i;
+      mw[i >> 5] |= sel ? 1u << (i & 31) : 0u;
     }
-    or_bits(wrow, j0, m);
   }
+  or_bits_w<NW>(wrow, j0, mw);
 }
 
 template <int TPR>
@@ -607,9 +619,13 @@ __device__ __forceinline__ void affinity_tiles(
 // Four waves per SIMD (at most 128 registers): the per-row bisection is a
 // chain of dependent VALU steps and reductions, and more resident waves hide
 // its latency better than the registers an unconstrained allocation keeps.
-template <bool F32, int D, int TPR>
-__global__ __launch_bounds__(kSelThreads)
-__attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
+// RV: a lane's values held in registers. The long form (RV > kRegVals,
+// histories of up to 16 RV blocks at 16 lanes per row) needs about 80 KB of
+// LDS per work-group, which already limits a CU to two of them, so it takes
+// up to 256 registers at two waves per SIMD.
+template <bool F32, int D, int TPR, int RV>
+__global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(
+    RV > kRegVals ? 2 : 4, RV > kRegVals ? 2 : 4))) void select_kernel(
     const DevPlan pl, const Workspace ws, const SelCall sc) {
   constexpr int RPW = kSelThreads / TPR;          // rows per pass
   constexpr int NRG = RPW >= 32 ? RPW / 32 : 1;   // 32-row MFMA groups
@@ -687,8 +703,8 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void select_kernel(
         const int cnt = max(0, min(L, nh - j0));  // real entries
         float* const my = ev + rr * stride + j0;
         uint32_t* const wrow = wb + row * W;
-        if (L <= kRegVals)
-          retain_row_regs<TPR>(my, L, nh, j0, sc.tau, lane, part, wrow);
+        if (L <= RV)
+          retain_row_regs<TPR, RV>(my, L, nh, j0, sc.tau, lane, part, wrow);
         else
           retain_row_lds<TPR>(my, L, cnt, nh, j0, sc.tau, lane, part, wrow);
       }
@@ -915,10 +931,10 @@ __global__ void seg_fill_kernel(float* __restrict__ p, size_t n) {
     p[i] = neg_inf();
 }
 
-template <bool F32, int D, int TPR>
+template <bool F32, int D, int TPR, int RV = kRegVals>
 hipError_t launch_sel(const DevPlan& p, const Workspace& w, const SelCall& c,
                       size_t lds, hipStream_t s) {
-  auto* fn = select_kernel<F32, D, TPR>;
+  auto* fn = select_kernel<F32, D, TPR, RV>;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(
         (const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -933,14 +949,19 @@ template <bool F32, int D>
 hipError_t launch_sel_d(const DevPlan& p, const Workspace& w,
                         const SelCall& c, int nh_max, hipStream_t s) {
   // fewest lanes per row whose share of the longest history fits in
-  // registers (and whose LDS lets two work-groups share a CU); else the
-  // LDS-streaming variant with the widest rows that fit
+  // registers (and whose LDS lets two work-groups share a CU); else 16 lanes
+  // per row with the long register form; else the LDS-streaming variant
+  // with the widest rows that fit
   const int tprs[3] = {4, 8, 16};
   int pick = -1;
   for (int i = 0; i < 3 && pick < 0; ++i)
     if (sel_per_thread(nh_max, tprs[i]) <= kRegVals &&
         sel_lds_bytes(nh_max, tprs[i], p.W, D) <= kSelLdsTwoPerCu)
       pick = i;
+  if (pick < 0 && sel_per_thread(nh_max, 16) <= kRegValsLong &&
+      sel_lds_bytes(nh_max, 16, p.W, D) <= kSelLdsTwoPerCu)
+    return launch_sel<F32, D, 16, kRegValsLong>(
+        p, w, c, sel_lds_bytes(nh_max, 16, p.W, D), s);
   for (int i = 0; i < 3 && pick < 0; ++i)
     if (sel_lds_bytes(nh_max, tprs[i], p.W, D) <= kSelLdsTwoPerCu) pick = i;
   for (int i = 0; i < 3 && pick < 0; ++i)
