@@ -354,13 +354,25 @@ def test_topp_skips_tiles_and_is_deterministic():
     np.testing.assert_array_equal(res.E, res2.E)
 
 
-def test_topp_long_history_streams_from_lds():
-    # 600 visual blocks: a row's share of its history no longer fits the
-    # register variant, so the retention streams it from LDS
+def test_topp_long_history_register_form():
+    # 600 visual blocks: a row's share of its history (38 entries at 16
+    # lanes per row) exceeds the common register form, so the long form
+    # (up to 72 entries per lane, two waves per SIMD) runs it
     w = _small("long-history", d=64, hq=2, hkv=1, tokens_per_frame=64,
                n_frames=(600,), n_text=(40,), n_sys=(6,), tau_p=TAU,
                key_struct=(1.0, 1.0, 0.9))
-    say("case long history")
+    say("case long history, long register form")
+    _run_case(w, rows_budget=256)
+
+
+def test_topp_very_long_history_streams_from_lds():
+    # 1,200 visual blocks: 76 entries per lane exceed the long register
+    # form too, so the retention streams each row's share from LDS (one
+    # work-group per CU)
+    w = _small("very-long-history", d=64, hq=2, hkv=1, tokens_per_frame=64,
+               n_frames=(1200,), n_text=(40,), n_sys=(6,), tau_p=TAU,
+               key_struct=(1.0, 1.0, 0.9))
+    say("case very long history, LDS-streaming retention")
     _run_case(w, rows_budget=256)
 
 
