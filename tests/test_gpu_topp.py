@@ -320,6 +320,17 @@ def test_topp_equal_affinity_runs():
     np.testing.assert_array_equal(kg, ref["keep"])
 
 
+def test_topp_equal_affinity_runs_long_register_form():
+    # the same tie rule in the long register form (600-block histories, 38
+    # entries per lane, three mask words per lane)
+    w = _small("dup-keys-long", d=64, hq=2, hkv=1, tokens_per_frame=64,
+               n_frames=(600,), n_text=(40,), n_sys=(0,), tau_p=TAU)
+    say("case duplicated key blocks, long register form")
+    _, keeps = _run_case(w, rows_budget=256, transform=_dup_key_blocks)
+    ref, kg, _, _ = keeps[0]
+    np.testing.assert_array_equal(kg, ref["keep"])
+
+
 def test_topp_underflowing_probabilities():
     w = _small("scaled-q", tokens_per_frame=64, n_frames=(120,),
                n_text=(64,), n_sys=(2,), tau_p=TAU)
