@@ -365,14 +365,15 @@ def test_topp_skips_tiles_and_is_deterministic():
     np.testing.assert_array_equal(res.E, res2.E)
 
 
-def test_topp_long_history_register_form():
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_topp_long_history_register_form(dtype):
     # 600 visual blocks: a row's share of its history (38 entries at 16
     # lanes per row) exceeds the common register form, so the long form
     # (up to 72 entries per lane, two waves per SIMD) runs it
     w = _small("long-history", d=64, hq=2, hkv=1, tokens_per_frame=64,
                n_frames=(600,), n_text=(40,), n_sys=(6,), tau_p=TAU,
-               key_struct=(1.0, 1.0, 0.9))
-    say("case long history, long register form")
+               key_struct=(1.0, 1.0, 0.9), dtype=dtype)
+    say(f"case long history, long register form, {dtype}")
     _run_case(w, rows_budget=256)
 
 
