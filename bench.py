@@ -258,6 +258,20 @@ def coarse_main(args, ev, w, mask, qs, kks, evid, e_qf, kk, topk, ws,
     step(evs)
     torch.cuda.synchronize()
     layer_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    # the retention alone (mean keys + per-row selection) per layer, from
+    # one further pass of evisel_select_blocks calls, each bracketed
+    st = mask.stats
+    rb = torch.empty((w.hq, st["n_blocks"], st["hist_words"], 64),
+                     dtype=torch.int32, device="cuda")
+    ub = torch.empty((w.hq, st["n_blocks"], st["hist_words"]),
+                     dtype=torch.int32, device="cuda")
+    for l in range(L):
+        evs[l][0].record(stream)
+        ev.select_blocks(mask, qs[l], kks[l], rb, ub, ws,
+                         softmax_scale=w.softmax_scale, stream=stream)
+        evs[l][1].record(stream)
+    torch.cuda.synchronize()
+    sel_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
     flop, nbytes = coarse_work(ev, mask, w)
     found = sorted(topk[:sum(ks)].cpu().numpy().tolist())
     rec = {
@@ -280,6 +294,7 @@ def coarse_main(args, ev, w, mask, qs, kks, evid, e_qf, kk, topk, ws,
                    "block": w.block, "tau_p": w.tau_p,
                    "parallelism": "single-gpu"},
         "coarse": {"ms_per_layer": layer_ms,
+                   "retention_ms_per_layer": sel_ms,
                    "algorithmic_flop_per_layer": flop,
                    "algorithmic_bytes_per_layer": nbytes,
                    "achieved_TFLOPs": flop / (layer_ms * 1e-3) / 1e12,
