@@ -61,12 +61,19 @@ struct PipeArgs {
   int64_t segtot;
   int32_t hq, hkv, Nv, S;
   float c2;       // softmax scale * log2(e)
+  // frame cues (the kernel's CUE form): visual rows' log2 partial masses
+  // per key frame of each computed visual tile at its CSR position, or
+  // null, and the log2 LSE of every non-query row, or null
+  float* segv;
+  float* lse2v;
+  int32_t nnz;
 };
 
 // A key tile as the loop sees it (wave-uniform).
 struct Tile {
   int start, len, region, aux;
   bool act;   // some row of this wave's half attends to it
+  int pos;    // CSR position of the tile for this half (CUE form only)
 };
 
 // Instruction order requested from the scheduler (sched_group_barrier
@@ -123,7 +130,7 @@ __device__ __forceinline__ void sched_block2() {
   }
 }
 
-template <int D>
+template <int D, bool CUE>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
                           amdgpu_waves_per_eu(2, 2))) void
 attn_pipe_kernel(const PipeArgs a) {
@@ -162,7 +169,7 @@ attn_pipe_kernel(const PipeArgs a) {
 
   // Tile descriptors, 64 at a time: lane t holds tile 64 * batch + t's
   // first token, aux field and (length | region << 8 | active << 10).
-  int dsc_start = 0, dsc_aux = 0, dsc_meta = 1;
+  int dsc_start = 0, dsc_aux = 0, dsc_meta = 1, dsc_pos = -1;
   auto load_batch = [&](int batch) {
     const int t = batch * 64 + lane;
     if (t < n) {
@@ -171,6 +178,7 @@ attn_pipe_kernel(const PipeArgs a) {
       dsc_start = bd.start;
       dsc_aux = bd.aux;
       dsc_meta = bd.len | bd.region << 8 | act << 10;
+      if (CUE) dsc_pos = uni ? a.ptile[b0 + t].pos[hsub] : b0 + t;
     }
   };
   auto desc = [&](int t) {
@@ -182,9 +190,10 @@ attn_pipe_kernel(const PipeArgs a) {
     d.len = meta & 255;
     d.region = (meta >> 8) & 3;
     d.act = (meta >> 10) & 1;
+    d.pos = CUE ? __builtin_amdgcn_readlane(dsc_pos, l) : -1;
     return d;
   };
-  const Tile none = {0, 1, 0, 0, false};
+  const Tile none = {0, 1, 0, 0, false, -1};
 
   TileLoader<__bf16, D, kSwzK> kload;
   TileLoader<__bf16, D, kSwzV> vload;
@@ -344,6 +353,30 @@ attn_pipe_kernel(const PipeArgs a) {
     }
   };
 
+  // Frame cues (CUE form): a visual row's log2 partial mass on each key
+  // frame of a computed visual tile, written at the tile's CSR position
+  // ([h][nnz][64 / N_v][64 rows]); frames hold 32 or 64 keys, h0 and h1 are
+  // the row's sums over keys 0-31 and 32-63.
+  const bool vis_ff =
+      CUE && a.segv != nullptr && !is_text && qb.region == kVis;
+  float* const segv_row =
+      vis_ff ? a.segv + (size_t)h * a.nnz * (kTile / a.Nv) * kTile + qrow
+             : nullptr;
+  auto vis_tile_halves = [&](const Tile& t, float h0, float h1) {
+    if (!vis_ff || t.region != kVis || t.pos < 0) return;
+    if (a.Nv == kTile) {
+      const float s = pair_sum(h0 + h1);
+      if (g == 0 && qvalid) segv_row[(size_t)t.pos * kTile] = m_ref + log2_(s);
+    } else {
+      const float s0 = pair_sum(h0), s1 = pair_sum(h1);
+      if (g == 0 && qvalid) {
+        float* const dst = segv_row + (size_t)t.pos * 2 * kTile;
+        dst[0] = m_ref + log2_(s0);
+        if (t.len > 32) dst[kTile] = m_ref + log2_(s1);
+      }
+    }
+  };
+
   // Exact recomputation of the whole item (row max per tile, accumulators
   // rescaled when it rises by more than kRescaleSlack), used when some row's
   // probabilities exceeded 2^64 against its first-tile reference.
@@ -417,6 +450,9 @@ attn_pipe_kernel(const PipeArgs a) {
         for (int q = 0; q < 8; ++q) ts += g8[q];
         l_part += ts;
         if (TXT) text_tile(cur, g8);
+        if (CUE && !TXT)
+          vis_tile_halves(cur, g8[0] + g8[1] + g8[2] + g8[3],
+                          g8[4] + g8[5] + g8[6] + g8[7]);
         pv_tile(vb0 + pt * TB, pb);
       }
       cur = nxt;
@@ -457,6 +493,7 @@ attn_pipe_kernel(const PipeArgs a) {
     auto finish = [&](const Tile& t, float h1) {
       const float ts = th + h1;
       if (TXT && t.act) text_tile_halves(t, th, h1);
+      if (CUE && !TXT && t.act) vis_tile_halves(t, th, h1);
       bad = bad || __any(active && !(ts <= kFastBound));
       l_part += ts;
     };
@@ -595,6 +632,8 @@ attn_pipe_kernel(const PipeArgs a) {
                     hh ? it.q1len : it.q0len, hh ? hd1 : it.head, a.hq, tid);
     if (qvalid && g == 0 && a.lse)
       a.lse[(size_t)h * a.S + qpos] = (m_ref + log2_(l_tot)) * kLn2;
+    if (CUE && qvalid && g == 0 && a.lse2v)
+      a.lse2v[(size_t)h * a.S + qpos] = m_ref + log2_(l_tot);
   } else if (active) {
     const float nv_tot = pair_sum(nv_part);
     const int slot =
@@ -622,7 +661,9 @@ attn_pipe_kernel(const PipeArgs a) {
 }  // namespace
 
 bool attention_pipe_supported(const DevPlan& p, const AttnCall& c) {
-  return !c.fp32 && !p.topp && c.segv == nullptr && c.lse2v == nullptr &&
+  // frame cues: frames of 32 or 64 keys (the loop keeps two half-tile sums)
+  const bool cues = c.segv != nullptr || c.lse2v != nullptr;
+  return !c.fp32 && !p.topp && (!cues || p.Nv >= 32) &&
          (c.d == 64 || c.d == 128);
 }
 
@@ -652,11 +693,19 @@ hipError_t launch_attention_pipe(const DevPlan& p, const Workspace& w,
   a.Nv = p.Nv;
   a.S = p.S;
   a.c2 = c.scale_log2;
+  a.segv = c.segv;
+  a.lse2v = c.lse2v;
+  a.nnz = p.nnz;
+  const bool cue = c.segv != nullptr || c.lse2v != nullptr;
   dim3 grid(p.n_items), block(kThreads);
-  if (c.d == 64)
-    attn_pipe_kernel<64><<<grid, block, 0, s>>>(a);
+  if (c.d == 64 && cue)
+    attn_pipe_kernel<64, true><<<grid, block, 0, s>>>(a);
+  else if (c.d == 64)
+    attn_pipe_kernel<64, false><<<grid, block, 0, s>>>(a);
+  else if (cue)
+    attn_pipe_kernel<128, true><<<grid, block, 0, s>>>(a);
   else
-    attn_pipe_kernel<128><<<grid, block, 0, s>>>(a);
+    attn_pipe_kernel<128, false><<<grid, block, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -31,7 +31,10 @@ WAIT_STATES = 5
 # SGPR spills per kernel at the current sources (kernel name fragment ->
 # spills); none of the pipelined kernel's is reloaded inside its tile loop
 SGPR_SPILL_BUDGET = {
-    "attn_pipe_kernelILi128": 86, "attn_pipe_kernelILi64": 95,
+    "attn_pipe_kernelILi128ELb0": 86, "attn_pipe_kernelILi64ELb0": 95,
+    # the pipelined kernel's frame-cue form (tile CSR positions in the
+    # descriptors, visual-row partials and LSE)
+    "attn_pipe_kernelILi128ELb1": 89, "attn_pipe_kernelILi64ELb1": 84,
     "attn_kernelINS0_8Bf16PathILi128EEELi128ELb0": 93,
     "attn_kernelINS0_8Bf16PathILi128EEELi128ELb1": 104,
     "attn_kernelINS0_8Bf16PathILi64EEELi64ELb0": 92,
