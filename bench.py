@@ -76,10 +76,12 @@ def measured_traffic():
 
 def attention_kernel_name(w, args):
     """The attention kernel the library launches for this run: the
-    pipelined kernel for bf16 inputs under the static rule without frame
-    cues, attn_kernel otherwise."""
-    if w.dtype == "bf16" and w.tau_p == 0 and not args.cues:
-        return f"attn_pipe_kernel<{w.d}>"
+    pipelined kernel for bf16 inputs under the static rule (its frame-cue
+    form with the cues, for frames of 32 or 64 keys), attn_kernel
+    otherwise."""
+    if w.dtype == "bf16" and w.tau_p == 0 and (not args.cues or
+                                               w.tokens_per_frame >= 32):
+        return f"attn_pipe_kernel<{w.d}, {'true' if args.cues else 'false'}>"
     path = "Bf16Path" if w.dtype == "bf16" else "F32Path"
     return f"attn_kernel<{path}<{w.d}>, {w.d}, {'true' if w.tau_p > 0 else 'false'}>"
 
